@@ -1,0 +1,169 @@
+"""Pins of the attention oracle against facts the mathematics fixes.
+
+Each pin takes an implementation with the oracle's signature
+``attn(q, k, v, mask, T, scale)`` (float64 arrays [B, H, F*T, d], F x F mask)
+and raises AssertionError when it disagrees. None of them re-runs the oracle's
+own formula: they compare against torch's CPU scaled_dot_product_attention
+(a library routine), a pure-Python brute force without the max shift, closed
+forms, and invariances of the definition (Sec. 3.3 of the paper).
+"""
+from __future__ import annotations
+
+import itertools
+import math
+
+import numpy as np
+import torch
+
+TOL = 1e-12
+
+
+def _rand(rng, B, H, S, d, scale=1.0):
+    return rng.standard_normal((B, H, S, d)) * scale
+
+
+def _sdpa_masked(q, k, v, mask, T, scale):
+    """Masked attention by torch SDPA with a token-level boolean mask; empty rows -> 0."""
+    F = mask.shape[0]
+    frame = np.arange(F * T) // T
+    tok = np.asarray(mask, dtype=bool)[frame][:, frame]  # [S, S]
+    qt, kt, vt = (torch.from_numpy(np.ascontiguousarray(x)) for x in (q, k, v))
+    empty = ~tok.any(axis=1)
+    tok_safe = tok.copy()
+    tok_safe[empty, :] = True  # avoid all-masked rows inside SDPA
+    out = torch.nn.functional.scaled_dot_product_attention(
+        qt, kt, vt, attn_mask=torch.from_numpy(tok_safe), scale=scale
+    ).numpy()
+    out[:, :, empty, :] = 0.0
+    return out
+
+
+def pin_dense_matches_sdpa(attn):
+    rng = np.random.default_rng(1)
+    for (B, H, F, T, d) in [(1, 2, 3, 5, 8), (2, 1, 2, 7, 4), (1, 1, 1, 9, 16)]:
+        q, k, v = (_rand(rng, B, H, F * T, d) for _ in range(3))
+        scale = 1 / math.sqrt(d)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            *(torch.from_numpy(x) for x in (q, k, v)), scale=scale).numpy()
+        got = attn(q, k, v, np.ones((F, F), np.uint8), T, scale)
+        assert np.max(np.abs(got - ref)) < TOL, "dense mask differs from textbook attention"
+
+
+def pin_all_small_masks_match_sdpa(attn):
+    """Every one of the 2^(F*F) masks for F <= 3 against library attention."""
+    rng = np.random.default_rng(2)
+    for F, T, d in [(1, 4, 4), (2, 3, 4), (3, 2, 4)]:
+        q, k, v = (_rand(rng, 1, 1, F * T, d) for _ in range(3))
+        for bits in itertools.product((0, 1), repeat=F * F):
+            mask = np.array(bits, dtype=np.uint8).reshape(F, F)
+            got = attn(q, k, v, mask, T, 0.7)
+            ref = _sdpa_masked(q, k, v, mask, T, 0.7)
+            assert np.max(np.abs(got - ref)) < TOL, f"mask {bits} differs"
+
+
+def pin_random_masks_match_sdpa(attn):
+    rng = np.random.default_rng(3)
+    for trial in range(6):
+        F = int(rng.integers(2, 6))
+        T = int(rng.choice([1, 3, 17]))
+        d = int(rng.choice([4, 16]))
+        B, H = 1 + trial % 2, 2
+        mask = (rng.random((F, F)) < 0.5).astype(np.uint8)
+        q, k, v = (_rand(rng, B, H, F * T, d) for _ in range(3))
+        scale = float(rng.uniform(0.1, 1.5))
+        got = attn(q, k, v, mask, T, scale)
+        ref = _sdpa_masked(q, k, v, mask, T, scale)
+        assert np.max(np.abs(got - ref)) < TOL
+
+
+def pin_bruteforce(attn):
+    """Pure-Python loops over tokens, normalising sum(exp) directly (no max shift)."""
+    rng = np.random.default_rng(4)
+    F, T, d = 3, 4, 3
+    mask = np.array([[1, 0, 1], [0, 0, 0], [1, 1, 0]], dtype=np.uint8)
+    q, k, v = (_rand(rng, 1, 1, F * T, d, 0.5) for _ in range(3))
+    scale = 0.9
+    got = attn(q, k, v, mask, T, scale)
+    for s in range(F * T):
+        kept = [t for t in range(F * T) if mask[s // T][t // T]]
+        if not kept:
+            expect = [0.0] * d
+        else:
+            w = {t: math.exp(scale * sum(q[0, 0, s, c] * k[0, 0, t, c] for c in range(d))) for t in kept}
+            z = sum(w.values())
+            expect = [sum(w[t] * v[0, 0, t, c] for t in kept) / z for c in range(d)]
+        assert max(abs(got[0, 0, s, c] - expect[c]) for c in range(d)) < TOL, f"row {s}"
+
+
+def pin_constant_values(attn):
+    """Softmax weights sum to one: V constant per column reproduces the constant."""
+    rng = np.random.default_rng(5)
+    F, T, d = 4, 6, 8
+    mask = (rng.random((F, F)) < 0.6).astype(np.uint8)
+    mask[2, :] = 0
+    q, k = (_rand(rng, 1, 2, F * T, d) for _ in range(2))
+    c = rng.standard_normal(d)
+    v = np.broadcast_to(c, (1, 2, F * T, d)).copy()
+    got = attn(q, k, v, mask, T, 0.5)
+    for s in range(F * T):
+        expect = c if mask[s // T].any() else np.zeros(d)
+        assert np.max(np.abs(got[0, :, s] - expect)) < TOL
+
+
+def pin_uniform_weights(attn):
+    """Q = 0 (or scale = 0) gives equal weights: the mean of V over the kept frames."""
+    rng = np.random.default_rng(6)
+    F, T, d = 4, 5, 6
+    mask = np.array([[1, 1, 0, 0], [0, 1, 0, 1], [0, 0, 0, 0], [1, 1, 1, 1]], dtype=np.uint8)
+    k, v = (_rand(rng, 1, 1, F * T, d) for _ in range(2))
+    frame_mean = v[0, 0].reshape(F, T, d).mean(axis=1)
+    for q, scale in [(np.zeros_like(k), 0.8), (_rand(rng, 1, 1, F * T, d), 0.0)]:
+        got = attn(q, k, v, mask, T, scale)
+        for i in range(F):
+            kept = np.flatnonzero(mask[i])
+            expect = frame_mean[kept].mean(axis=0) if len(kept) else np.zeros(d)
+            assert np.max(np.abs(got[0, 0, i * T:(i + 1) * T] - expect)) < TOL
+
+
+def pin_identical_frames(attn):
+    """If every frame's K/V is the same copy, any mask with a kept tile per row equals
+    attention over that one frame (repeating keys leaves softmax unchanged)."""
+    rng = np.random.default_rng(7)
+    F, T, d = 4, 6, 8
+    k1, v1 = (_rand(rng, 1, 1, T, d) for _ in range(2))
+    k, v = np.tile(k1, (1, 1, F, 1)), np.tile(v1, (1, 1, F, 1))
+    q = _rand(rng, 1, 1, F * T, d)
+    mask = np.eye(F, dtype=np.uint8)
+    mask[:, 0] = 1
+    mask[3, :] = 1
+    got = attn(q, k, v, mask, T, 0.6)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k1), torch.from_numpy(v1), scale=0.6).numpy()
+    assert np.max(np.abs(got - ref)) < TOL
+
+
+def pin_key_frame_permutation(attn):
+    """Relabelling key frames (K/V frames and mask columns together) changes nothing."""
+    rng = np.random.default_rng(8)
+    F, T, d = 5, 3, 4
+    q, k, v = (_rand(rng, 1, 1, F * T, d) for _ in range(3))
+    mask = (rng.random((F, F)) < 0.5).astype(np.uint8)
+    mask[np.arange(F), np.arange(F)] = 1
+    perm = rng.permutation(F)
+    kp = k.reshape(1, 1, F, T, d)[:, :, perm].reshape(1, 1, F * T, d)
+    vp = v.reshape(1, 1, F, T, d)[:, :, perm].reshape(1, 1, F * T, d)
+    a = attn(q, k, v, mask, T, 0.8)
+    b = attn(q, kp, vp, mask[:, perm], T, 0.8)
+    assert np.max(np.abs(a - b)) < TOL
+
+
+ALL_PINS = [
+    pin_dense_matches_sdpa,
+    pin_all_small_masks_match_sdpa,
+    pin_random_masks_match_sdpa,
+    pin_bruteforce,
+    pin_constant_values,
+    pin_uniform_weights,
+    pin_identical_frames,
+    pin_key_frame_permutation,
+]
