@@ -1,0 +1,124 @@
+/*
+ * tile_attn.h -- C ABI of the gfx950 (MI355X) tile-sparse 3D attention library.
+ *
+ * Operation (Efficient-vDiT, arXiv 2502.06155, Sec. 3.1 and Sec. 3.3): a video
+ * token sequence of S = F * T tokens is flattened frame-major (Sec. 4.1), so
+ * token s belongs to latent frame s / T. A frame-level F x F tile mask decides,
+ * for each query frame i, which key frames j it attends to. For a query token s
+ * of frame i,
+ *
+ *     out[s] = sum_t softmax_t(scale * <q[s], k[t]>) * v[t]
+ *
+ * over the key tokens t of the kept frames only; a query frame with no kept key
+ * frame produces zeros. Tiles the mask drops are never read or computed (the
+ * block skipping of App. B), so work grows with the number of kept tiles, which
+ * for the k:(F-k) masks (diagonal plus k global reference frames) is linear in F.
+ *
+ * Conventions shared by all entry points:
+ *   - q, k, v, out are DEVICE pointers to bf16 values (raw 16-bit storage),
+ *     contiguous [B, H, S, d] with S = F * T, frame-major tokens, each pointer
+ *     16-byte aligned. out must not overlap q, k or v. The caller owns them.
+ *   - Accumulation is fp32 (QK^T and PV on bf16 matrix cores, softmax state in
+ *     fp32); out is rounded to bf16 with round-to-nearest-even.
+ *   - d (head dimension) must be 64, 96 or 128. B, H, F, T >= 1,
+ *     F <= TA_MAX_FRAMES, S <= 2^31 - 1; offsets are 64-bit.
+ *   - scale must be finite; 1/sqrt(d) is the usual choice. Any sign is allowed.
+ *   - stream is a hipStream_t passed as void*; NULL means the null stream. The
+ *     call is asynchronous: it enqueues the kernel and returns.
+ *   - Argument errors are detected before any HIP call: the status is returned
+ *     and nothing is enqueued. A HIP failure returns TA_ERR_HIP; the detail is in
+ *     tile_attn_last_error().
+ *   - Thread-safe. The first call for a given mask (per device) uploads its
+ *     compact kept-tile list with a blocking allocation and copy; later calls
+ *     with the same mask allocate nothing and do not synchronise, so a warmed-up
+ *     call can be captured in a HIP graph.
+ */
+#ifndef TILE_ATTN_H
+#define TILE_ATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TA_MAX_FRAMES 1024
+
+typedef enum {
+  TA_OK = 0,
+  TA_ERR_NULL_PTR = 1,  /* a required pointer is NULL */
+  TA_ERR_BAD_SHAPE = 2, /* B, H, F, T out of range, S or the grid overflows */
+  TA_ERR_HEAD_DIM = 3,  /* d is not 64, 96 or 128 */
+  TA_ERR_BAD_MASK = 4,  /* mask recipe out of range (tile_attn_make_mask) */
+  TA_ERR_ALIGN = 5,     /* a tensor pointer is not 16-byte aligned */
+  TA_ERR_BAD_SCALE = 6, /* scale is NaN or infinite */
+  TA_ERR_OVERLAP = 7,   /* out overlaps q, k or v */
+  TA_ERR_HIP = 8        /* a HIP runtime call or the launch failed */
+} ta_status;
+
+/* Mask forms for tile_attn_make_mask. */
+typedef enum {
+  TA_MASK_COL = 0,  /* query frame i keeps key frame i and every global frame */
+  TA_MASK_SYM = 1,  /* TA_MASK_COL, plus every global query frame keeps all frames */
+  TA_MASK_DENSE = 2 /* every tile kept (3D full attention) */
+} ta_mask_form;
+
+/*
+ * Tile-sparse attention forward (Sec. 3.3; kernel-only benchmark of Sec. 4.2.1:
+ * inputs query, key, value and mask, output the attention output).
+ *
+ * tile_mask: HOST pointer to F*F bytes, row-major [query_frame][key_frame];
+ * nonzero = tile kept. It is read during the call only. The mask is
+ * authoritative: no diagonal is added.
+ */
+int tile_attn_fwd(const void* q, const void* k, const void* v, void* out,
+                  int B, int H, int F, int T, int d,
+                  const uint8_t* tile_mask, float scale, void* stream);
+
+/*
+ * Dense control: 3D full attention (every tile kept, the "full" rows of
+ * tab:kernel_time). Runs the same kernel as tile_attn_fwd with an all-ones
+ * mask, so its output is bit-identical to tile_attn_fwd with that mask.
+ */
+int dense_attn_fwd(const void* q, const void* k, const void* v, void* out,
+                   int B, int H, int F, int T, int d, float scale, void* stream);
+
+/*
+ * Build a k:(F-k) mask (Sec. 3.3): the main diagonal plus k global reference
+ * frames chosen uniformly, frames 0, s, 2s, ... below F with s = ceil(F / k)
+ * (fewer than k frames when the stride overshoots). form selects how the
+ * reference frames are kept (ta_mask_form). With TA_MASK_SYM this placement
+ * reproduces every sparsity printed in tab:kernel_time.
+ *
+ * mask_out: HOST buffer of F*F bytes, written row-major with 0/1.
+ * Errors: TA_ERR_NULL_PTR, TA_ERR_BAD_SHAPE (F outside 1..TA_MAX_FRAMES),
+ * TA_ERR_BAD_MASK (k outside 0..F or unknown form). Touches no GPU.
+ */
+int tile_attn_make_mask(int F, int k, int form, uint8_t* mask_out);
+
+/*
+ * The compact kept-tile list the kernels walk instead of the dense mask
+ * (App. B: masked blocks are skipped and the full mask is never materialised).
+ *
+ * row_ptr: HOST int32[F+1]; kept key frames of query frame i are
+ *   cols[row_ptr[i] .. row_ptr[i+1]), ascending.
+ * cols: HOST uint16[F*F] (capacity F*F; the first *nnz entries are written).
+ * order: HOST uint16[F]; query frames by descending kept-tile count (ties by
+ *   frame index), the order in which work is dispatched. May be NULL.
+ * nnz: HOST int, receives the number of kept tiles.
+ * Errors: TA_ERR_NULL_PTR, TA_ERR_BAD_SHAPE. Touches no GPU.
+ */
+int tile_attn_compact(const uint8_t* tile_mask, int F, int32_t* row_ptr,
+                      uint16_t* cols, uint16_t* order, int* nnz);
+
+/* Static text for a status code. */
+const char* tile_attn_status_string(int status);
+
+/* Detail of the last error on the calling thread (empty string if none). */
+const char* tile_attn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TILE_ATTN_H */

@@ -1,0 +1,18 @@
+"""Tile-sparse 3D attention forward for MI355X (gfx950).
+
+The hot path of Efficient-vDiT (arXiv 2502.06155): softmax attention in which
+each query latent frame only attends to the key frames its frame-tile mask
+keeps (diagonal plus k global reference frames), computed by hand-written HIP
+kernels behind a C ABI (include/tile_attn.h). This package is the thin Python
+binding of that ABI.
+"""
+from .api import (  # noqa: F401
+    MASK_FORMS,
+    TileAttnError,
+    dense_attn,
+    dense_attn_fwd,
+    tile_attn,
+    tile_attn_compact,
+    tile_attn_fwd,
+    tile_attn_make_mask,
+)

@@ -1,0 +1,136 @@
+"""Python binding of the C ABI in include/tile_attn.h (argument marshalling only).
+
+Every function forwards to the HIP library; all attention arithmetic runs in
+the gfx950 kernels. PyTorch is used only to read device pointers and the
+current stream of tensors handed in by the caller.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+
+from ._lib import lib
+
+TA_OK = 0
+MASK_FORMS = {"col": 0, "sym": 1, "dense": 2}
+
+
+class TileAttnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        text = lib.tile_attn_status_string(status).decode()
+        detail = lib.tile_attn_last_error().decode()
+        super().__init__(f"{where}: {text} ({status}): {detail}")
+
+
+def _check(status: int, where: str) -> None:
+    if status != TA_OK:
+        raise TileAttnError(status, where)
+
+
+def _ptr(x) -> int | None:
+    """Device address of a torch tensor, or an integer address as given."""
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    return int(x)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return None
+    if hasattr(stream, "cuda_stream"):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _mask_bytes(tile_mask, F: int) -> np.ndarray:
+    m = np.ascontiguousarray(np.asarray(tile_mask), dtype=np.uint8)
+    if m.size != F * F:
+        raise ValueError(f"tile_mask must hold F*F = {F * F} entries, got {m.size}")
+    return m
+
+
+def tile_attn_fwd(q, k, v, out, B: int, H: int, F: int, T: int, d: int, tile_mask,
+                  scale: float, stream=None) -> None:
+    """tile_attn_fwd of the C ABI. q, k, v, out: device tensors or addresses."""
+    m = _mask_bytes(tile_mask, F)
+    _check(lib.tile_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, F, T, d,
+                             m.ctypes.data, float(scale), _stream(stream)), "tile_attn_fwd")
+
+
+def dense_attn_fwd(q, k, v, out, B: int, H: int, F: int, T: int, d: int, scale: float,
+                   stream=None) -> None:
+    """dense_attn_fwd of the C ABI: every tile kept."""
+    _check(lib.dense_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, F, T, d,
+                              float(scale), _stream(stream)), "dense_attn_fwd")
+
+
+def tile_attn_make_mask(F: int, k: int, form: str | int = "col") -> np.ndarray:
+    """k:(F-k) mask as an F x F uint8 array (tile_attn_make_mask of the C ABI)."""
+    f = MASK_FORMS[form] if isinstance(form, str) else int(form)
+    out = np.zeros((F, F), dtype=np.uint8) if F >= 1 else np.zeros(1, dtype=np.uint8)
+    _check(lib.tile_attn_make_mask(F, k, f, out.ctypes.data), "tile_attn_make_mask")
+    return out
+
+
+def tile_attn_compact(tile_mask):
+    """Kept-tile list of a mask: (row_ptr int32[F+1], cols uint16[nnz], order uint16[F])."""
+    m = np.asarray(tile_mask)
+    F = m.shape[0]
+    m = _mask_bytes(m, F)
+    row_ptr = np.zeros(F + 1, dtype=np.int32)
+    cols = np.zeros(F * F, dtype=np.uint16)
+    order = np.zeros(F, dtype=np.uint16)
+    nnz = ctypes.c_int(0)
+    _check(lib.tile_attn_compact(m.ctypes.data, F, row_ptr.ctypes.data, cols.ctypes.data,
+                                 order.ctypes.data, ctypes.byref(nnz)), "tile_attn_compact")
+    return row_ptr, cols[: nnz.value].copy(), order
+
+
+def _shape_of(q, T: int):
+    if q.dim() != 4:
+        raise ValueError("expected [B, H, S, d] tensors")
+    B, H, S, d = q.shape
+    if S % T:
+        raise ValueError(f"S = {S} is not a multiple of T = {T}")
+    return B, H, S // T, d
+
+
+def _check_tensors(*ts):
+    import torch
+
+    for t in ts:
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous bfloat16 on a GPU")
+
+
+def tile_attn(q, k, v, tile_mask, T: int, scale: float | None = None, out=None):
+    """Torch convenience wrapper: [B, H, F*T, d] bf16 tensors on the current stream."""
+    import torch
+
+    B, H, F, d = _shape_of(q, T)
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensors(q, k, v, out)
+    if scale is None:
+        scale = d ** -0.5
+    tile_attn_fwd(q, k, v, out, B, H, F, T, d, tile_mask, scale,
+                  torch.cuda.current_stream(q.device))
+    return out
+
+
+def dense_attn(q, k, v, T: int, scale: float | None = None, out=None):
+    """Torch convenience wrapper of the dense control."""
+    import torch
+
+    B, H, F, d = _shape_of(q, T)
+    if out is None:
+        out = torch.empty_like(q)
+    _check_tensors(q, k, v, out)
+    if scale is None:
+        scale = d ** -0.5
+    dense_attn_fwd(q, k, v, out, B, H, F, T, d, scale, torch.cuda.current_stream(q.device))
+    return out

@@ -1,0 +1,226 @@
+// C-ABI entry points: argument checks, the k:(F-k) mask builder, compaction of
+// the frame mask into a kept-tile list, a per-device cache of that list, and
+// dispatch of the gfx950 kernel on the caller's stream.
+#include "../../include/tile_attn.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const std::string& detail) {
+  g_last_error = detail;
+  return status;
+}
+
+// Kept-tile list of one mask, resident on one device.
+struct DeviceKeptList {
+  void* buffer = nullptr;  // [row_ptr int32 F+1][order uint16 F][cols uint16 nnz]
+  const int32_t* row_ptr = nullptr;
+  const uint16_t* order = nullptr;
+  const uint16_t* cols = nullptr;
+  int nnz = 0;
+};
+
+std::mutex g_cache_mutex;
+std::map<std::pair<int, std::string>, DeviceKeptList> g_cache;
+
+void compact_host(const uint8_t* mask, int F, int32_t* row_ptr, uint16_t* cols,
+                  uint16_t* order, int* nnz_out) {
+  int nnz = 0;
+  row_ptr[0] = 0;
+  for (int i = 0; i < F; ++i) {
+    for (int j = 0; j < F; ++j)
+      if (mask[(size_t)i * F + j]) cols[nnz++] = (uint16_t)j;
+    row_ptr[i + 1] = nnz;
+  }
+  if (order) {
+    std::vector<int> idx(F);
+    std::iota(idx.begin(), idx.end(), 0);
+    std::stable_sort(idx.begin(), idx.end(), [&](int a, int b) {
+      return row_ptr[a + 1] - row_ptr[a] > row_ptr[b + 1] - row_ptr[b];
+    });
+    for (int i = 0; i < F; ++i) order[i] = (uint16_t)idx[i];
+  }
+  *nnz_out = nnz;
+}
+
+bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  auto x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+int check_args(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
+               int T, int d, float scale) {
+  if (!q || !k || !v || !out) return fail(TA_ERR_NULL_PTR, "q, k, v and out must be non-NULL");
+  if (B < 1 || H < 1 || F < 1 || T < 1)
+    return fail(TA_ERR_BAD_SHAPE, "B, H, F and T must be >= 1");
+  if (F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F exceeds TA_MAX_FRAMES");
+  if ((int64_t)F * T > INT32_MAX) return fail(TA_ERR_BAD_SHAPE, "F * T exceeds 2^31 - 1");
+  if (d != 64 && d != 96 && d != 128) return fail(TA_ERR_HEAD_DIM, "d must be 64, 96 or 128");
+  const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
+  const int64_t n_wg = (int64_t)B * H * F * nqb;
+  if (n_wg * ta::kThreads > (int64_t)UINT32_MAX)
+    return fail(TA_ERR_BAD_SHAPE, "B * H * F * ceil(T / 128) workgroups exceed the grid limit");
+  if (!std::isfinite(scale)) return fail(TA_ERR_BAD_SCALE, "scale must be finite");
+  for (const void* p : {q, k, v, (const void*)out})
+    if (reinterpret_cast<uintptr_t>(p) % 16)
+      return fail(TA_ERR_ALIGN, "q, k, v and out must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * F * T * d * 2;
+  for (const void* p : {q, k, v})
+    if (ranges_overlap(out, bytes, p, bytes)) return fail(TA_ERR_OVERLAP, "out overlaps an input");
+  return TA_OK;
+}
+
+// Returns the device-resident kept list for `mask`, uploading it on first use.
+int kept_list_for(const uint8_t* mask, int F, const DeviceKeptList** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  std::string key(reinterpret_cast<const char*>(mask), (size_t)F * F);
+  std::lock_guard<std::mutex> lock(g_cache_mutex);
+  auto it = g_cache.find({dev, key});
+  if (it != g_cache.end()) {
+    *out = &it->second;
+    return TA_OK;
+  }
+  std::vector<int32_t> row_ptr(F + 1);
+  std::vector<uint16_t> cols((size_t)F * F + 1), order(F);
+  int nnz = 0;
+  compact_host(mask, F, row_ptr.data(), cols.data(), order.data(), &nnz);
+  const size_t off_order = sizeof(int32_t) * (F + 1);
+  const size_t off_cols = off_order + sizeof(uint16_t) * F;
+  const size_t total = off_cols + sizeof(uint16_t) * std::max(nnz, 1);
+  std::vector<uint8_t> host(total, 0);
+  std::memcpy(host.data(), row_ptr.data(), off_order);
+  std::memcpy(host.data() + off_order, order.data(), sizeof(uint16_t) * F);
+  std::memcpy(host.data() + off_cols, cols.data(), sizeof(uint16_t) * nnz);
+  void* buf = nullptr;
+  e = hipMalloc(&buf, total);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
+  e = hipMemcpy(buf, host.data(), total, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(buf);
+    return fail(TA_ERR_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
+  }
+  DeviceKeptList entry;
+  entry.buffer = buf;
+  entry.row_ptr = static_cast<const int32_t*>(buf);
+  entry.order = reinterpret_cast<const uint16_t*>(static_cast<uint8_t*>(buf) + off_order);
+  entry.cols = reinterpret_cast<const uint16_t*>(static_cast<uint8_t*>(buf) + off_cols);
+  entry.nnz = nnz;
+  auto res = g_cache.emplace(std::make_pair(dev, std::move(key)), entry);
+  *out = &res.first->second;
+  return TA_OK;
+}
+
+int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F, int T,
+            int d, const uint8_t* mask, float scale, void* stream) {
+  const DeviceKeptList* kl = nullptr;
+  int st = kept_list_for(mask, F, &kl);
+  if (st != TA_OK) return st;
+  ta::FwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.out = static_cast<uint16_t*>(out);
+  a.B = B;
+  a.H = H;
+  a.F = F;
+  a.T = T;
+  a.d = d;
+  a.row_ptr = kl->row_ptr;
+  a.cols = kl->cols;
+  a.order = kl->order;
+  a.c = std::fabs(scale) * 1.4426950408889634f;
+  a.qflip = std::signbit(scale) ? 0x80008000u : 0u;
+  a.n_wg = (uint32_t)((int64_t)B * H * F * ((T + ta::kBlockQ - 1) / ta::kBlockQ));
+  hipError_t e = ta::launch_tile_attn_fwd(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  g_last_error.clear();
+  return TA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tile_attn_make_mask(int F, int k, int form, uint8_t* mask_out) {
+  if (!mask_out) return fail(TA_ERR_NULL_PTR, "mask_out must be non-NULL");
+  if (F < 1 || F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F must be in 1..TA_MAX_FRAMES");
+  if (k < 0 || k > F) return fail(TA_ERR_BAD_MASK, "k must be in 0..F");
+  if (form != TA_MASK_COL && form != TA_MASK_SYM && form != TA_MASK_DENSE)
+    return fail(TA_ERR_BAD_MASK, "unknown mask form");
+  std::memset(mask_out, form == TA_MASK_DENSE ? 1 : 0, (size_t)F * F);
+  if (form == TA_MASK_DENSE) return TA_OK;
+  // Reference frames 0, s, 2s, ... with s = ceil(F / k).
+  std::vector<char> is_global(F, 0);
+  if (k > 0) {
+    const int stride = (F + k - 1) / k;
+    for (int j = 0; j < F; j += stride) is_global[j] = 1;
+  }
+  for (int i = 0; i < F; ++i) {
+    uint8_t* row = mask_out + (size_t)i * F;
+    const bool full_row = form == TA_MASK_SYM && is_global[i];
+    for (int j = 0; j < F; ++j) row[j] = (full_row || i == j || is_global[j]) ? 1 : 0;
+  }
+  return TA_OK;
+}
+
+int tile_attn_compact(const uint8_t* tile_mask, int F, int32_t* row_ptr, uint16_t* cols,
+                      uint16_t* order, int* nnz) {
+  if (!tile_mask || !row_ptr || !cols || !nnz)
+    return fail(TA_ERR_NULL_PTR, "tile_mask, row_ptr, cols and nnz must be non-NULL");
+  if (F < 1 || F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F must be in 1..TA_MAX_FRAMES");
+  compact_host(tile_mask, F, row_ptr, cols, order, nnz);
+  return TA_OK;
+}
+
+int tile_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
+                  int T, int d, const uint8_t* tile_mask, float scale, void* stream) {
+  int st = check_args(q, k, v, out, B, H, F, T, d, scale);
+  if (st != TA_OK) return st;
+  if (!tile_mask) return fail(TA_ERR_NULL_PTR, "tile_mask must be non-NULL");
+  return run_fwd(q, k, v, out, B, H, F, T, d, tile_mask, scale, stream);
+}
+
+int dense_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
+                   int T, int d, float scale, void* stream) {
+  int st = check_args(q, k, v, out, B, H, F, T, d, scale);
+  if (st != TA_OK) return st;
+  std::vector<uint8_t> ones((size_t)F * F, 1);
+  return run_fwd(q, k, v, out, B, H, F, T, d, ones.data(), scale, stream);
+}
+
+const char* tile_attn_status_string(int status) {
+  switch (status) {
+    case TA_OK: return "ok";
+    case TA_ERR_NULL_PTR: return "null pointer";
+    case TA_ERR_BAD_SHAPE: return "bad shape";
+    case TA_ERR_HEAD_DIM: return "unsupported head dimension";
+    case TA_ERR_BAD_MASK: return "bad mask recipe";
+    case TA_ERR_ALIGN: return "misaligned pointer";
+    case TA_ERR_BAD_SCALE: return "non-finite scale";
+    case TA_ERR_OVERLAP: return "output overlaps an input";
+    case TA_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* tile_attn_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,226 @@
+"""Parity of the gfx950 HIP path with the float64 oracle (needs an MI355X).
+
+Every call goes through the C ABI (via the ctypes binding). Small problems are
+compared element by element against the full oracle; the measured workloads are
+run at full size in the benchmark's launch configuration and compared on
+sampled rows that the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import attention as oa
+from oracle import masks as om
+from tests.gpu_helpers import assert_parity, errors, from_dev, sample_rows, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2502_06155_amd as ta  # noqa: E402
+
+
+def run_gpu(qb, kb, vb, mask, T, scale, dense=False):
+    B, H, S, d = qb.shape
+    F = S // T
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+    if dense:
+        ta.dense_attn_fwd(q, k, v, out, B, H, F, T, d, scale, stream)
+    else:
+        ta.tile_attn_fwd(q, k, v, out, B, H, F, T, d, mask, scale, stream)
+    torch.cuda.synchronize()
+    return from_dev(out)
+
+
+def full_check(qb, kb, vb, mask, T, scale, what):
+    print(f"[case] {what} shape={qb.shape} T={T}", flush=True)
+    got = run_gpu(qb, kb, vb, mask, T, scale)
+    ref = oa.attention(qb, kb, vb, mask, T, scale)
+    return assert_parity(got, ref, what)
+
+
+@pytest.mark.parametrize("form", ["col", "sym", "dense"])
+def test_tiny_workload(form):
+    w = workloads.WORKLOADS["tiny"]
+    qb, kb, vb = workloads.make_workload_qkv(w)
+    full_check(qb, kb, vb, om.tile_mask(w.F, w.g, form), w.T, w.scale(), f"tiny-{form}")
+
+
+@pytest.mark.parametrize("d", [64, 96, 128])
+@pytest.mark.parametrize("T", [1, 15, 16, 17, 31, 33, 63, 64, 65, 127, 128, 129, 200, 257])
+def test_ragged_tails(d, T):
+    F = 3
+    B, H = 1, 2
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=T * 7 + d)
+    mask = np.array([[1, 0, 1], [1, 1, 0], [0, 1, 1]], np.uint8)
+    full_check(qb, kb, vb, mask, T, d ** -0.5, f"tails-d{d}-T{T}")
+
+
+@pytest.mark.parametrize("d", [64, 96, 128])
+def test_multi_tile_random_masks(d):
+    rng = np.random.default_rng(d)
+    B, H, F, T = 2, 3, 5, 300
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=d, dist="frame_shift")
+    for trial in range(3):
+        mask = (rng.random((F, F)) < 0.45).astype(np.uint8)
+        mask[trial, :] = 0  # an empty row: zeros
+        full_check(qb, kb, vb, mask, T, d ** -0.5, f"random-d{d}-{trial}")
+
+
+def test_empty_rows_are_zero():
+    B, H, F, T, d = 1, 2, 4, 100, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=3)
+    mask = om.tile_mask(F, 1, "col")
+    mask[2, :] = 0
+    got = run_gpu(qb, kb, vb, mask, T, d ** -0.5)
+    assert np.all(got[:, :, 2 * T:3 * T] == 0)
+
+
+def test_frame_tail_keys_are_used():
+    """Spike V on the keys past the last full 64-key tile of each frame: a kernel that
+    dropped the ragged frame tail would pass the absolute gate at random inputs but
+    not here."""
+    B, H, F, T, d = 1, 2, 4, 3600, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=11)
+    v = workloads.bf16_bits_to_f32(vb).reshape(B, H, F, T, d)
+    v[:, :, :, T - 16:, :] += 8.0
+    vb = workloads.f32_to_bf16_bits(v.reshape(B, H, F * T, d))
+    mask = om.tile_mask(F, 1, "col")
+    got = run_gpu(qb, kb, vb, mask, T, d ** -0.5)
+    b, h, s = sample_rows(B, H, F, T, per_frame=8)
+    ref = oa.attention_rows(qb, kb, vb, mask, T, d ** -0.5, b, h, s)
+    assert_parity(got[b, h, s], ref, "tail-spike")
+
+
+def test_skipped_tiles_are_never_read():
+    """Poison the K/V of frames the mask skips with NaN and 1e30: rows that do not
+    keep the poisoned frames must not change by a single bit, which shows those
+    tiles are skipped rather than masked. T = 200 leaves a ragged 8-key tail in
+    every frame, so a tail load running into the next frame would be caught."""
+    B, H, F, T, d = 1, 2, 6, 200, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=5)
+    mask = om.tile_mask(F, 2, "col")  # G = {0, 3}
+    base = run_gpu(qb, kb, vb, mask, T, d ** -0.5)
+    for poisoned_frames in ([4], [1, 5], [2, 4]):
+        kp, vp = kb.copy(), vb.copy()
+        for j in poisoned_frames:
+            kp[:, :, j * T:(j + 1) * T] = 0x7FC0  # NaN
+            vp[:, :, j * T:(j + 1) * T] = 0x7149  # about 1e30
+        got = run_gpu(qb, kp, vp, mask, T, d ** -0.5)
+        clean = [i for i in range(F) if not any(mask[i, j] for j in poisoned_frames)]
+        assert clean
+        for i in clean:
+            assert np.array_equal(got[:, :, i * T:(i + 1) * T], base[:, :, i * T:(i + 1) * T]), i
+    ref = oa.attention(qb, kb, vb, mask, T, d ** -0.5)
+    assert_parity(base, ref, "poison-base")
+
+
+def test_dense_control_is_bitwise_all_ones_mask():
+    B, H, F, T, d = 1, 3, 4, 300, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=9)
+    a = run_gpu(qb, kb, vb, None, T, d ** -0.5, dense=True)
+    b = run_gpu(qb, kb, vb, np.ones((F, F), np.uint8), T, d ** -0.5)
+    assert np.array_equal(a, b)
+    assert_parity(a, oa.attention(qb, kb, vb, np.ones((F, F)), T, d ** -0.5), "dense")
+
+
+def test_repeat_calls_are_bitwise_equal():
+    B, H, F, T, d = 1, 4, 8, 500, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=2)
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    mask = om.tile_mask(F, 2, "sym")
+    outs = []
+    for _ in range(3):
+        o = torch.empty_like(q)
+        ta.tile_attn_fwd(q, k, v, o, B, H, F, T, d, mask, d ** -0.5)
+        outs.append(o)
+    torch.cuda.synchronize()
+    assert all(torch.equal(outs[0], o) for o in outs[1:])
+
+
+def test_non_default_stream():
+    B, H, F, T, d = 1, 2, 4, 256, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=4)
+    mask = om.tile_mask(F, 1, "col")
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        out = torch.empty_like(q)
+        ta.tile_attn_fwd(q, k, v, out, B, H, F, T, d, mask, d ** -0.5, s)
+    s.synchronize()
+    assert_parity(from_dev(out), oa.attention(qb, kb, vb, mask, T, d ** -0.5), "stream")
+
+
+def test_output_guard_bands_untouched():
+    B, H, F, T, d = 1, 2, 3, 129, 128
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=6)
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    n = q.numel()
+    guard = 4096
+    big = torch.full((n + 2 * guard,), 1.2345, dtype=torch.bfloat16, device="cuda")
+    out = big[guard:guard + n].view(B, H, F * T, d)
+    mask = om.tile_mask(F, 1, "sym")
+    ta.tile_attn_fwd(q, k, v, out, B, H, F, T, d, mask, d ** -0.5)
+    torch.cuda.synchronize()
+    g = from_dev(big)
+    canary = from_dev(torch.tensor([1.2345], dtype=torch.bfloat16))[0]
+    assert np.all(g[:guard] == canary) and np.all(g[guard + n:] == canary)
+    assert_parity(from_dev(out), oa.attention(qb, kb, vb, mask, T, d ** -0.5), "guard")
+
+
+@pytest.mark.parametrize("scale", [-0.1, 0.0, 0.35, 2.0])
+def test_scale_values(scale):
+    B, H, F, T, d = 1, 2, 3, 150, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=12)
+    mask = om.tile_mask(F, 1, "col")
+    full_check(qb, kb, vb, mask, T, scale, f"scale{scale}")
+
+
+def test_many_frames_short_tiles():
+    """F above 255 exercises 16-bit kept lists; T = 2 puts many frames in one tile."""
+    B, H, F, T, d = 1, 1, 300, 2, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=13)
+    mask = om.tile_mask(F, 7, "sym")
+    full_check(qb, kb, vb, mask, T, d ** -0.5, "F300")
+
+
+# ---- measured workloads at full size, sampled rows --------------------------------
+
+_CACHE = {}
+
+
+def _inputs(w):
+    key = (w.B, w.H, w.F, w.T, w.d, w.seed, w.dist)
+    if key not in _CACHE:
+        _CACHE.clear()
+        _CACHE[key] = workloads.make_workload_qkv(w)
+    return _CACHE[key]
+
+
+FULL_CASES = [
+    ("29f", "col", 1), ("29f", "sym", 1), ("29f", "dense", 1),
+    ("93f", "col", 1), ("93f", "sym", 1), ("93f", "dense", 1),
+    ("sweep", "col", 2), ("sweep", "sym", 2), ("sweep", "col", 4), ("sweep", "sym", 8),
+    ("sweep", "dense", 1),
+    ("sp_share", "col", 1), ("long", "col", 2), ("long", "sym", 2),
+]
+
+
+@pytest.mark.parametrize("name,form,g", FULL_CASES, ids=[f"{a}-{b}-g{c}" for a, b, c in FULL_CASES])
+def test_full_size_sampled(name, form, g):
+    w = workloads.WORKLOADS[name]
+    print(f"[case] full {name} {form} g={g}", flush=True)
+    qb, kb, vb = _inputs(w)
+    mask = om.tile_mask(w.F, g, form)
+    got = run_gpu(qb, kb, vb, mask, w.T, w.scale())
+    heads = None if form != "dense" else [0, w.H // 2, w.H - 1]
+    b, h, s = sample_rows(w.B, w.H, w.F, w.T, per_frame=2, heads=heads, seed=len(name))
+    ref = oa.attention_rows(qb, kb, vb, mask, w.T, w.scale(), b, h, s)
+    assert_parity(got[b, h, s], ref, f"{name}-{form}-g{g}")
+    # rows of frames that keep nothing do not exist in these masks; outputs are finite
+    assert errors(got[:, :, :: max(1, w.T // 7)], np.zeros(1))["finite"]
