@@ -16,10 +16,11 @@ struct FwdArgs {
   uint16_t* out;
   int B, H, F, T, d;
   const int32_t* row_ptr;  // device, F + 1
-  const uint16_t* cols;    // device, nnz
-  const uint16_t* order;   // device, F: dispatch order of query frames
-  float c;                 // |scale| * log2(e): logits in base-2 units
+  const int32_t* cols;     // device, nnz: kept key frames, row after row
+  const int32_t* order;    // device, F: dispatch order of query frames
+  float c;                 // > 0: |scale| * log2(e), logits in base-2 units
   uint32_t qflip;          // 0x80008000 flips the sign of q (negative scale), else 0
+  uint32_t qmask;          // 0 zeroes q (scale 0: exactly uniform weights), else ~0
   uint32_t n_wg;           // B * H * F * ceil(T / kBlockQ)
 };
 

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cfloat>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -27,12 +28,13 @@ int fail(int status, const std::string& detail) {
   return status;
 }
 
-// Kept-tile list of one mask, resident on one device.
+// Kept-tile list of one mask, resident on one device, in 32-bit words so the
+// kernels read it with scalar loads.
 struct DeviceKeptList {
-  void* buffer = nullptr;  // [row_ptr int32 F+1][order uint16 F][cols uint16 nnz]
+  void* buffer = nullptr;  // [row_ptr int32 F+1][order int32 F][cols int32 nnz]
   const int32_t* row_ptr = nullptr;
-  const uint16_t* order = nullptr;
-  const uint16_t* cols = nullptr;
+  const int32_t* order = nullptr;
+  const int32_t* cols = nullptr;
   int nnz = 0;
 };
 
@@ -102,17 +104,19 @@ int kept_list_for(const uint8_t* mask, int F, const DeviceKeptList** out) {
   std::vector<uint16_t> cols((size_t)F * F + 1), order(F);
   int nnz = 0;
   compact_host(mask, F, row_ptr.data(), cols.data(), order.data(), &nnz);
-  const size_t off_order = sizeof(int32_t) * (F + 1);
-  const size_t off_cols = off_order + sizeof(uint16_t) * F;
-  const size_t total = off_cols + sizeof(uint16_t) * std::max(nnz, 1);
-  std::vector<uint8_t> host(total, 0);
-  std::memcpy(host.data(), row_ptr.data(), off_order);
-  std::memcpy(host.data() + off_order, order.data(), sizeof(uint16_t) * F);
-  std::memcpy(host.data() + off_cols, cols.data(), sizeof(uint16_t) * nnz);
+  std::vector<int32_t> words;
+  words.reserve((size_t)2 * F + 1 + std::max(nnz, 1));
+  words.insert(words.end(), row_ptr.begin(), row_ptr.end());
+  const size_t off_order = words.size();
+  words.insert(words.end(), order.begin(), order.end());
+  const size_t off_cols = words.size();
+  words.insert(words.end(), cols.begin(), cols.begin() + nnz);
+  if (nnz == 0) words.push_back(0);
+  const size_t total = words.size() * sizeof(int32_t);
   void* buf = nullptr;
   e = hipMalloc(&buf, total);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
-  e = hipMemcpy(buf, host.data(), total, hipMemcpyHostToDevice);
+  e = hipMemcpy(buf, words.data(), total, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(buf);
     return fail(TA_ERR_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
@@ -120,8 +124,8 @@ int kept_list_for(const uint8_t* mask, int F, const DeviceKeptList** out) {
   DeviceKeptList entry;
   entry.buffer = buf;
   entry.row_ptr = static_cast<const int32_t*>(buf);
-  entry.order = reinterpret_cast<const uint16_t*>(static_cast<uint8_t*>(buf) + off_order);
-  entry.cols = reinterpret_cast<const uint16_t*>(static_cast<uint8_t*>(buf) + off_cols);
+  entry.order = static_cast<const int32_t*>(buf) + off_order;
+  entry.cols = static_cast<const int32_t*>(buf) + off_cols;
   entry.nnz = nnz;
   auto res = g_cache.emplace(std::make_pair(dev, std::move(key)), entry);
   *out = &res.first->second;
@@ -146,8 +150,18 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   a.row_ptr = kl->row_ptr;
   a.cols = kl->cols;
   a.order = kl->order;
-  a.c = std::fabs(scale) * 1.4426950408889634f;
-  a.qflip = std::signbit(scale) ? 0x80008000u : 0u;
+  // Logits are formed from |scale| (a negative scale flips the sign of q, which
+  // is exact in bf16). scale == 0 zeroes q instead, so every logit is exactly 0
+  // and the weights exactly uniform; c only has to stay positive.
+  if (scale == 0.f) {
+    a.c = 1.f;
+    a.qflip = 0u;
+    a.qmask = 0u;
+  } else {
+    a.c = std::max(std::fabs(scale) * 1.4426950408889634f, FLT_MIN);
+    a.qflip = std::signbit(scale) ? 0x80008000u : 0u;
+    a.qmask = 0xFFFFFFFFu;
+  }
   a.n_wg = (uint32_t)((int64_t)B * H * F * ((T + ta::kBlockQ - 1) / ta::kBlockQ));
   hipError_t e = ta::launch_tile_attn_fwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
