@@ -27,8 +27,9 @@ import workloads  # noqa: E402
 
 # MI355X dense bf16 matrix peak: 256 CUs x 4096 FLOP/clk x 2.4 GHz (the published 2.5 PFLOP/s).
 PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12
-KERNEL_SRC = os.path.join(ROOT, "paper_2502_06155_amd", "csrc", "tile_attn_kernels.hip")
-PMC_FILE = os.path.join(ROOT, "profiles", "tile_attn_fwd_93f_col_g1.pmc.json")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2502_06155_amd", "csrc", f)
+               for f in ("tile_attn_kernels.hip", "launch.h")]
+PROFILE_MD = os.path.join(ROOT, "profiles", "tile_attn_fwd_93f_col_g1.md")
 
 
 def log(*a):
@@ -67,16 +68,21 @@ def paper_stat(per_call):
 
 
 def traffic_from_profile():
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
-    taken on the current kernel source; else None."""
-    if not os.path.exists(PMC_FILE):
+    """HBM bytes per launch of the attention kernel from the committed rocprofv3
+    counter summary (FETCH_SIZE and WRITE_SIZE, each calibrated on a plain copy of
+    known size), or None when the summary was taken on other kernel sources."""
+    if not os.path.exists(PROFILE_MD):
         return None
-    with open(PMC_FILE) as f:
-        rec = json.load(f)
-    sha = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if rec.get("kernel_sha256") != sha:
+    rec = {}
+    with open(PROFILE_MD) as f:
+        for line in f:
+            if ":" in line and not line.startswith(("|", "#", " ", "`")):
+                key, _, val = line.partition(":")
+                rec[key.strip()] = val.strip()
+    sha = hashlib.sha256(b"".join(open(p, "rb").read() for p in KERNEL_SRCS)).hexdigest()
+    if rec.get("kernel_sha256") != sha or "hbm_bytes_per_launch" not in rec:
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return float(rec["hbm_bytes_per_launch"])
 
 
 def cpu_baseline(w, qb, kb, vb, mask, budget_s: float):
@@ -120,7 +126,14 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="counter pass: sparse calls, then a plain copy of --copy-mib MiB "
+                         "(the calibration kernel for HBM byte counters); no dense, no CPU")
+    ap.add_argument("--copy-mib", type=int, default=1024)
     args = ap.parse_args()
+    if args.profile_pass:
+        args.no_dense = True
+        args.no_cpu_baseline = True
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the attention "
@@ -162,6 +175,17 @@ def main():
     tflops = flop / (ms * 1e-3) / 1e12
     log(f"[bench] sparse: {ms:.3f} ms/call (median {med:.3f}, P20-P80 {band:.3f}), "
         f"{tflops:.1f} TFLOP/s kept, nnz {nnz}/{w.F * w.F}")
+
+    if args.profile_pass:
+        # A plain elementwise copy that reads and writes exactly copy_mib MiB each: the
+        # same HBM counters read on it give the factor from counter units to bytes.
+        n = args.copy_mib * (1 << 20) // 2
+        src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: 3 x torch.neg over {args.copy_mib} MiB in, {args.copy_mib} MiB out")
 
     extra = {}
     if not args.no_dense:
