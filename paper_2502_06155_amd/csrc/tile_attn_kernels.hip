@@ -18,24 +18,34 @@
 //   C (32 x 32): lane l holds col l%32, rows 8*i + 4*(l/32) + j at index 4*i + j
 //   The kernel computes S^T = K * Q^T (A = K rows from LDS, B = this wave's 32
 //   queries held in registers), so each lane owns ONE query and 16 of every 32
-//   keys: the softmax row max and row sum are in-lane reductions plus a single
-//   exchange with lane l^32. The probabilities P^T then sit exactly where the
-//   B operand of O^T += V^T * P^T expects them (contraction over keys), and only
-//   V needs a transpose, done once per tile while staging it in LDS.
+//   keys. The probabilities P^T then sit exactly where the B operand of
+//   O^T += V^T * P^T expects them, with the contraction index k of chunk ch
+//   mapped to keys 16ch + 4h + (0..3) and 16ch + 8 + 4h + (0..3) for lane half h.
+//   The V^T operand is read from the untransposed V tile with the LDS transpose
+//   load ds_read_b64_tr_b16: inside each 16-lane group, lane i receives element
+//   i%4 of the 8-byte rows read by lanes 4k + i/4 (k = 0..3), so when lane j reads
+//   V[key0 + j/4][d0 + 4(j%4) .. +3], lane i gets V[key0 .. key0+3][d0 + i].
 //
 // Pipeline (one barrier per 64-key tile t)
-//   global loads of K(t+2) and V(t+1) are in flight while the wave computes
-//   S(t+1) = K(t+1) Q^T on the matrix cores and the softmax of S(t) on the
-//   vector ALUs (independent work the two units overlap), then O^T += V(t)^T P(t)^T.
-//   K and V each have two LDS buffers; K runs one tile ahead of V.
+//   Step t stores K(t+2) and V(t+1), loaded into registers during step t-1, into
+//   the LDS buffers that tiles t and t-1 freed, and starts the global loads of
+//   K(t+3) and V(t+2), which have a whole step to arrive. It then runs in two
+//   halves over 32-key blocks: QK^T of a block of tile t+1, the weights of the
+//   previous block and PV of the one before, three independent pieces whose
+//   MFMAs and VALU work interleave. K and V each have two LDS buffers; K runs one
+//   tile ahead of V.
 //
-// Online softmax (fp32, base 2): logits are scaled by c = |scale| * log2(e).
-// The exponent reference m_ref is only raised when a tile's max exceeds it by
-// more than 2^kLazyLog2 in weight; in between, weights may reach 2^kLazyLog2,
-// which fp32 and bf16 hold exactly as well as weights <= 1, and the rescale of
-// O^T and l is skipped. The result is the same softmax; only the reference of
-// the exponentials moves less often. The row sum l is accumulated from the
-// bf16-rounded weights that also feed the PV product.
+// Online softmax (fp32, base 2): weights are exp2(c * (s - m_ref)) with
+// c = |scale| * log2(e) and m_ref an exponent reference per query that only
+// moves when needed. The first tile sets m_ref to its row max. After that the
+// weights are formed directly; if any lane's sum of weights in a tile exceeds
+// 2^kLazyLog2 (so some weight may have grown past it), that tile is redone with
+// m_ref raised to the running max and O^T and l rescaled. Weights up to
+// 2^kLazyLog2 are as exact in fp32 and bf16 as weights up to 1, so the result is
+// the same softmax; only the reference of the exponentials moves less often. The
+// row sum l is accumulated from the bf16-rounded weights that also feed the PV
+// product, per lane (its 16 of every 32 keys) and summed over the two lane
+// halves once, in the epilogue.
 #include <hip/hip_runtime.h>
 
 #include <float.h>
@@ -49,30 +59,35 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kWaves = kThreads / 64;
 constexpr int kWaveQ = 32;   // query rows per wave: the N side of the 32x32 MFMA
 constexpr int kBlockK = 64;  // keys per K/V tile staged in LDS
-constexpr float kLazyLog2 = 8.f;
+constexpr float kLazyLog2 = 10.f;
 static_assert(kWaves * kWaveQ == kBlockQ, "workgroup rows");
 
 template <int D>
 struct Shape {
-  static constexpr int kStrideK = D + 8;        // LDS row stride of a K tile (bf16)
-  static constexpr int kStrideV = kBlockK + 8;  // LDS row stride of a V^T tile (bf16)
-  static constexpr int kChunks = D / 16;        // 16-wide slices of the QK^T contraction
-  static constexpr int kDBlocks = D / 32;       // 32-row blocks of O^T
-  static constexpr int kKVecs = kBlockK * D / 8;            // 16-byte pieces of a K tile
-  static constexpr int kKPerThread = (kKVecs + kThreads - 1) / kThreads;
-  static constexpr int kVGroups = (kBlockK / 4) * (D / 8);  // 4-key x 8-d pieces of a V tile
-  static_assert(kVGroups <= kThreads, "one V piece per thread");
+  // LDS row strides (bf16). K rows are read 16 bytes per lane, 16 rows at a time:
+  // D + 8 spreads those rows over all 64 banks. V rows are read 8 bytes per lane by
+  // the transpose load, 4 rows x 64 bytes at a time: a stride of 48 or 16 banks
+  // (mod 64) keeps those four rows apart.
+  static constexpr int kStrideK = D + 8;
+  static constexpr int kStrideV = (D % 64 == 32) ? D : D + 32;
+  static constexpr int kChunks = D / 16;   // 16-wide slices of the QK^T contraction
+  static constexpr int kDBlocks = D / 32;  // 32-row blocks of O^T
+  static constexpr int kPieces = D / 8;    // 16-byte pieces per K/V row
+  static constexpr int kPiecesPerThread = kBlockK * kPieces / kThreads;
+  static_assert(kBlockK * kPieces % kThreads == 0, "whole pieces per thread");
   static constexpr int kSizeK = kBlockK * kStrideK;
-  static constexpr int kSizeV = D * kStrideV;
+  static constexpr int kSizeV = kBlockK * kStrideV;
 };
 
 // Workgroup id -> logical work index such that the ids the hardware sends to
@@ -94,14 +109,6 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Position of a group of 4 keys (index kg within the 64-key tile) inside a
-// transposed V row. Each 16-key chunk is stored as keys 0-3, 8-11, 4-7, 12-15,
-// so the eight keys lane half h contracts over (4h..4h+3 and 8+4h..8+4h+3, the
-// C-layout rows it owns) are contiguous.
-__device__ __forceinline__ int vt_pos(int kg) {
-  return (kg >> 2) * 16 + ((kg & 1) << 3) + ((kg & 2) << 1);
-}
-
 // Walks the kept tiles of one query frame in order: tile (e, kt) covers keys
 // [64*kt, 64*kt + 64) of kept frame cols[e]. All state is wave-uniform (SGPRs);
 // the kept list is read with one scalar load per kept frame.
@@ -109,13 +116,13 @@ struct TileCursor {
   const int32_t* cols;  // kept frames of this query frame
   int e = 0, kt = 0, kf = 0;
   int tiles_per_frame, T;
-  __device__ __forceinline__ void start(const int32_t* c, int tpf, int t_len, int skip) {
+  __device__ __forceinline__ void start(const int32_t* c, int tpf, int t_len) {
     cols = c;
     tiles_per_frame = tpf;
     T = t_len;
-    e = skip / tpf;
-    kt = skip % tpf;
-    kf = cols[e];
+    e = 0;
+    kt = 0;
+    kf = cols[0];
   }
   __device__ __forceinline__ void advance(int n_frames) {
     if (++kt == tiles_per_frame) {
@@ -152,146 +159,119 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
+// Register staging of one 64-key K or V tile: the tile is kBlockK * D contiguous
+// bf16 in global memory, cut into 16-byte pieces; thread tid moves pieces
+// tid, tid + 256, ... into LDS rows of the given stride.
 template <int D>
-struct KStage {
-  static_assert(Shape<D>::kKVecs % kThreads == 0, "whole K pieces per thread");
-  u32x4 r[Shape<D>::kKPerThread];
-  __device__ __forceinline__ void load(const uint16_t* Kh, size_t key0, int nvalid, int tid) {
-    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(Kh + key0 * D, nvalid, D);
+struct Stage {
+  u32x4 r[Shape<D>::kPiecesPerThread];
+  __device__ __forceinline__ void load(const uint16_t* Xh, size_t key0, int nvalid, int tid) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(Xh + key0 * D, nvalid, D);
 #pragma unroll
-    for (int i = 0; i < Shape<D>::kKPerThread; ++i) {
-      const int idx = tid + i * kThreads;
-      const int row = idx / (D / 8), c8 = idx % (D / 8);
-      r[i] = buf_load16(rs, (row * D + 8 * c8) * 2);
-    }
+    for (int i = 0; i < Shape<D>::kPiecesPerThread; ++i)
+      r[i] = buf_load16(rs, (tid + i * kThreads) * 16);
   }
-  __device__ __forceinline__ void store(uint16_t* sK, int tid) const {
+  template <int STRIDE>
+  __device__ __forceinline__ void store(uint16_t* s, int tid) const {
 #pragma unroll
-    for (int i = 0; i < Shape<D>::kKPerThread; ++i) {
+    for (int i = 0; i < Shape<D>::kPiecesPerThread; ++i) {
       const int idx = tid + i * kThreads;
-      const int row = idx / (D / 8), c8 = idx % (D / 8);
-      *reinterpret_cast<u32x4*>(sK + row * Shape<D>::kStrideK + 8 * c8) = r[i];
+      const int row = idx / Shape<D>::kPieces, c8 = idx % Shape<D>::kPieces;
+      *reinterpret_cast<u32x4*>(s + row * STRIDE + 8 * c8) = r[i];
     }
   }
 };
 
+// S^T of 32-key block kb of a K tile (32 keys x 32 queries), raw logits.
 template <int D>
-struct VStage {
-  u32x4 r[4];  // 4 consecutive keys x 8 consecutive d
-  // Threads past kVGroups (whole waves) stage nothing.
-  __device__ __forceinline__ void load(const uint16_t* Vh, size_t key0, int nvalid, int tid) {
-    if (tid >= Shape<D>::kVGroups) return;
-    const int kg = tid % (kBlockK / 4), dg = tid / (kBlockK / 4);
-    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(Vh + key0 * D, nvalid, D);
+__device__ __forceinline__ f32x16 qk_block(const uint16_t* sK, const bf16x8 (&qf)[D / 16], int n,
+                                           int hf, int kb) {
+  const uint16_t* row = sK + (kb * 32 + n) * Shape<D>::kStrideK + 8 * hf;
+  f32x16 s = mfma32(as_bf16x8(load16(row)), qf[0], f32x16{});
 #pragma unroll
-    for (int j = 0; j < 4; ++j) r[j] = buf_load16(rs, ((4 * kg + j) * D + 8 * dg) * 2);
-  }
-  // Transpose 4 keys x 8 d into 8 rows of V^T (4 keys = 8 bytes each).
-  __device__ __forceinline__ void store(uint16_t* sV, int tid) const {
-    if (tid >= Shape<D>::kVGroups) return;
-    const int kg = tid % (kBlockK / 4), dg = tid / (kBlockK / 4);
-    const int pos = vt_pos(kg);
-#pragma unroll
-    for (int mm = 0; mm < 4; ++mm) {
-      u32x2 lo, hi;
-      lo[0] = __builtin_amdgcn_perm(r[1][mm], r[0][mm], 0x05040100u);
-      lo[1] = __builtin_amdgcn_perm(r[3][mm], r[2][mm], 0x05040100u);
-      hi[0] = __builtin_amdgcn_perm(r[1][mm], r[0][mm], 0x07060302u);
-      hi[1] = __builtin_amdgcn_perm(r[3][mm], r[2][mm], 0x07060302u);
-      *reinterpret_cast<u32x2*>(sV + (8 * dg + 2 * mm) * Shape<D>::kStrideV + pos) = lo;
-      *reinterpret_cast<u32x2*>(sV + (8 * dg + 2 * mm + 1) * Shape<D>::kStrideV + pos) = hi;
-    }
-  }
-};
+  for (int cc = 1; cc < D / 16; ++cc) s = mfma32(as_bf16x8(load16(row + 16 * cc)), qf[cc], s);
+  return s;
+}
 
-// S^T (64 keys x 32 queries) = K_tile * Q^T. In a frame's last tile the keys past
-// the frame end start from -inf, so they drop out of the max and get weight 0.
-template <int D>
-__device__ __forceinline__ void qk_tile(const uint16_t* sK, const bf16x8 (&qf)[D / 16], int n,
-                                        int hf, int nvalid, f32x16 (&s)[2]) {
-  if (nvalid < kBlockK) {
+// Keys of block kb past the frame end get -inf: no part in the max, weight 0.
+__device__ __forceinline__ void mask_tail(f32x16& s, int kb, int hf, int nvalid) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-        s[kb][r] = key < nvalid ? 0.f : -INFINITY;
-      }
-  } else {
-    s[0] = f32x16{};
-    s[1] = f32x16{};
-  }
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-    for (int cc = 0; cc < D / 16; ++cc) {
-      const bf16x8 a =
-          as_bf16x8(load16(sK + (kb * 32 + n) * Shape<D>::kStrideK + 16 * cc + 8 * hf));
-      s[kb] = mfma32(a, qf[cc], s[kb]);
-    }
+  for (int r = 0; r < 16; ++r) {
+    const int key = kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
+    if (key >= nvalid) s[r] = -INFINITY;
   }
 }
 
-// O^T (d x 32 queries) += V_tile^T * P^T.
+// V^T fragment (32 d-rows x 16 keys, A-operand layout) for d-block mb and key
+// chunk ch, from a V tile stored row-major (key, d) in LDS. Lane l: group
+// g = l/16, j = l%16 reads V[16ch + 4(g/2) + j/4 (+8)][32mb + 16(g%2) + 4(j%4) ..].
 template <int D>
-__device__ __forceinline__ void pv_tile(const uint16_t* sV, const bf16x8 (&pf)[4], int n, int hf,
-                                        f32x16 (&o)[D / 32]) {
-#pragma unroll
-  for (int ch = 0; ch < 4; ++ch)
-#pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) {
-      const bf16x8 a =
-          as_bf16x8(load16(sV + (mb * 32 + n) * Shape<D>::kStrideV + 16 * ch + 8 * hf));
-      o[mb] = mfma32(a, pf[ch], o[mb]);
-    }
+__device__ __forceinline__ bf16x8 vt_frag(const uint16_t* sV, int lane, int mb, int ch) {
+  const int g = lane >> 4, j = lane & 15;
+  const uint16_t* p =
+      sV + (16 * ch + 4 * (g >> 1) + (j >> 2)) * Shape<D>::kStrideV + 32 * mb + 16 * (g & 1) + 4 * (j & 3);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * Shape<D>::kStrideV));
+  const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  return as_bf16x8(u32x4{a[0], a[1], b[0], b[1]});
 }
 
-// Online softmax of one 64-key tile of S^T: updates the running state and
-// returns the bf16 weights in B-operand form (chunk ch = accumulator entries
-// 8*(ch%2)..+7 of key block ch/2, exactly this lane's 8 keys of that chunk).
-// c > 0 always (the host passes a tiny positive c for scale 0), so masked keys
-// (-inf) map to exp2(-inf) = 0.
+// O^T (d x 32 queries) += V^T * P^T over 32-key block kb (key chunks 2kb, 2kb+1).
 template <int D>
-__device__ __forceinline__ void softmax_tile(f32x16 (&s)[2], float c, float lazy_raw,
-                                             float& m_ref, float& l_run, f32x16 (&o)[D / 32],
-                                             bf16x8 (&pf)[4]) {
-  float mx = fmaxf(s[0][0], s[0][1]);
+__device__ __forceinline__ void pv_block(const uint16_t* sV, const bf16x8 (&p)[2], int lane, int kb,
+                                         f32x16 (&o)[D / 32]) {
 #pragma unroll
-  for (int r = 2; r < 16; r += 2) mx = fmaxf(fmaxf(mx, s[0][r]), s[0][r + 1]);
+  for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-  for (int r = 0; r < 16; r += 2) mx = fmaxf(fmaxf(mx, s[1][r]), s[1][r + 1]);
-  mx = pair_max(mx);
+    for (int mb = 0; mb < D / 32; ++mb)
+      o[mb] = mfma32(vt_frag<D>(sV, lane, mb, 2 * kb + c2), p[c2], o[mb]);
+}
 
-  // Raise the exponent reference only when some lane's weights would exceed 2^kLazyLog2.
-  if (__builtin_amdgcn_ballot_w64(mx - m_ref > lazy_raw) != 0) {
-    const float m_new = fmaxf(m_ref, mx);
-    const float alpha = fast_exp2((m_ref - m_new) * c);
-    l_run *= alpha;
+// This lane's max over its 16 scores of a block (-inf keys included).
+__device__ __forceinline__ float block_max(const f32x16& s) {
+  float mx = fmaxf(s[0], s[1]);
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-    m_ref = m_new;
-  }
-  const float mc = m_ref * c;
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s[kb][r] = fast_exp2(__builtin_fmaf(s[kb][r], c, -mc));
+  for (int r = 2; r < 16; r += 2) mx = fmaxf(fmaxf(mx, s[r]), s[r + 1]);
+  return mx;
+}
+
+// Weights exp2(c*s - mc) of one 32-key block in B-operand form (chunk c2 =
+// accumulator entries 8*c2 .. 8*c2+7, exactly this lane's 8 keys of that 16-key
+// chunk); returns this lane's sum of the bf16-rounded weights.
+__device__ __forceinline__ float block_weights(const f32x16& s, float c, float mc, bf16x8 (&p)[2]) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float ls = 0.f;
 #pragma unroll
-  for (int ch = 0; ch < 4; ++ch) {
-    const f32x16& sb = s[ch >> 1];
-    const int base = 8 * (ch & 1);
-    f32x8 x = {sb[base + 0], sb[base + 1], sb[base + 2], sb[base + 3],
-               sb[base + 4], sb[base + 5], sb[base + 6], sb[base + 7]};
-    pf[ch] = __builtin_convertvector(x, bf16x8);
+  for (int c2 = 0; c2 < 2; ++c2) {
+    f32x8 x;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = fast_exp2(__builtin_fmaf(s[8 * c2 + e], c, -mc));
+    p[c2] = __builtin_convertvector(x, bf16x8);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const bf16x2 pair = {pf[ch][2 * e], pf[ch][2 * e + 1]};
+      const bf16x2 pair = {p[c2][2 * e], p[c2][2 * e + 1]};
       ls = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, ls, false);
     }
   }
-  l_run += pair_sum(ls);
+  return ls;
+}
+
+// Scheduling hint for one half step: D/16 LDS reads and D/16 MFMAs of QK^T,
+// D/16 transposed-read pairs and D/16 MFMAs of PV, and the weights of one block
+// (about 50 VALU instructions). A few LDS reads go first, then each MFMA is
+// followed by a slice of the VALU work and the next LDS reads, so the vector
+// ALUs work while each MFMA runs.
+template <int D>
+__device__ __forceinline__ void interleave_half_step() {
+  constexpr int kMfma = 2 * (D / 16);
+  constexpr int kValu = 52 / kMfma + 1;
+  __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);  // DS read
+#pragma unroll
+  for (int i = 0; i < kMfma; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, kValu, 0);  // VALU
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);      // DS read
+  }
 }
 
 template <int D>
@@ -341,9 +321,9 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   f32x16 o[Sh::kDBlocks];
 #pragma unroll
   for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[mb] = f32x16{};
-  float m_ref = -FLT_MAX;  // exponent reference (raw logit units) of this lane's query
-  float l_run = 0.f;       // running sum of weights
-  const float lazy_raw = kLazyLog2 / c;
+  float m_ref = -INFINITY;  // exponent reference (raw logit units) of this lane's query
+  float l_run = 0.f;        // this lane's part of the running sum of weights
+  const float lazy = exp2f(kLazyLog2);
 
   const int kbeg = row_ptr[frame];
   const int n_kept = row_ptr[frame + 1] - kbeg;
@@ -351,59 +331,119 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   const int n_tiles = n_kept * tpf;
 
   if (n_tiles > 0) {
-    KStage<D> kst;
-    VStage<D> vst;
-    // kc points at tile t + 2 (next K to stage), vc at tile t + 1 (next V to stage).
+    Stage<D> kst, vst;
+    // Prologue: K(0), V(0) and K(1) into LDS, scores of tile 0, then the loads of
+    // K(2) and V(1), which step 0 stores.
     TileCursor kc, vc;
-    kc.start(cols + kbeg, tpf, T, 0);
+    kc.start(cols + kbeg, tpf, T);
     kst.load(Kh, kc.key0(), kc.nvalid(), tid);
     vst.load(Vh, kc.key0(), kc.nvalid(), tid);
     const int nv0 = kc.nvalid();
-    kst.store(sK[0], tid);
-    vst.store(sV[0], tid);
-    vc = kc;
-    vc.advance(n_kept);
-    if (n_tiles > 1) {
-      kc.advance(n_kept);
-      kst.load(Kh, kc.key0(), kc.nvalid(), tid);
-      kst.store(sK[1], tid);
-    }
+    kst.template store<Sh::kStrideK>(sK[0], tid);
+    vst.template store<Sh::kStrideV>(sV[0], tid);
     kc.advance(n_kept);
+    vc = kc;  // tile 1
+    if (n_tiles > 1) {
+      kst.load(Kh, kc.key0(), kc.nvalid(), tid);
+      kst.template store<Sh::kStrideK>(sK[1], tid);
+    }
+    kc.advance(n_kept);  // tile 2
     __syncthreads();
 
-    f32x16 sa[2], sb[2];
-    if (wave_active) qk_tile<D>(sK[0], qf, n, hf, nv0, sa);
-
-    // One pipeline step: softmax + PV of tile t (scores in s_cur), QK^T of
-    // tile t + 1 (into s_nxt), staging of K(t+2) and V(t+1).
-    auto step = [&](int t, f32x16(&s_cur)[2], f32x16(&s_nxt)[2]) {
-      const bool have_k2 = t + 2 < n_tiles, have_v1 = t + 1 < n_tiles;
-      if (have_k2) kst.load(Kh, kc.key0(), kc.nvalid(), tid);
-      if (have_v1) vst.load(Vh, vc.key0(), vc.nvalid(), tid);
-      if (wave_active) {
-        if (have_v1) qk_tile<D>(sK[(t + 1) & 1], qf, n, hf, vc.nvalid(), s_nxt);
-        bf16x8 pf[4];
-        softmax_tile<D>(s_cur, c, lazy_raw, m_ref, l_run, o, pf);
-        pv_tile<D>(sV[t & 1], pf, n, hf, o);
+    // Carried from one step to the next: the scores of the second block of tile
+    // t (sa/sb) and the weights and their lane sum of its first block (pa/pb, la/lb).
+    f32x16 sa, sb;
+    bf16x8 pa[2], pb[2];
+    float la = 0.f, lb = 0.f;
+    if (wave_active) {
+      f32x16 s0 = qk_block<D>(sK[0], qf, n, hf, 0);
+      sa = qk_block<D>(sK[0], qf, n, hf, 1);
+      if (nv0 < kBlockK) {
+        mask_tail(s0, 0, hf, nv0);
+        mask_tail(sa, 1, hf, nv0);
       }
-      if (have_k2) kst.store(sK[t & 1], tid);
-      if (have_v1) vst.store(sV[(t + 1) & 1], tid);
+      // The first tile sets the exponent reference.
+      m_ref = pair_max(fmaxf(block_max(s0), block_max(sa)));
+      la = block_weights(s0, c, m_ref * c, pa);
+    }
+    // Tiles that do not exist are loaded with an empty range (all zeros).
+    kst.load(Kh, kc.key0(), n_tiles > 2 ? kc.nvalid() : 0, tid);
+    vst.load(Vh, vc.key0(), n_tiles > 1 ? vc.nvalid() : 0, tid);
+    kc.advance(n_kept);  // tile 3
+    vc.advance(n_kept);  // tile 2
+    int kt_next = tpf > 1 ? 1 : 0;  // index within its frame of tile t + 1
+    // Step 0 overwrites K(0)'s buffer with K(2); every wave must be done reading it.
+    __syncthreads();
+
+    // Raise the exponent reference to cover block s, rescale what is accumulated
+    // so far, and redo the block's weights.
+    auto rescale = [&](const f32x16& s_blk, bf16x8(&p)[2], float& l) {
+      const float m_new = fmaxf(m_ref, pair_max(block_max(s_blk)));
+      const float alpha = fast_exp2((m_ref - m_new) * c);
+      l_run *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[mb] *= alpha;
+      m_ref = m_new;
+      l = block_weights(s_blk, c, m_ref * c, p);
+    };
+
+    // Step t, in two halves over 32-key blocks b = 2t, 2t+1:
+    //   half 0: QK^T of block 2t+2 (tile t+1), weights of block 2t+1, PV of block 2t
+    //   half 1: QK^T of block 2t+3 (tile t+1), weights of block 2t+2, PV of block 2t+1
+    // The three parts of a half are independent, so their MFMAs and VALU work
+    // interleave. Block b's weights are checked before its PV; a rescale at that
+    // point multiplies exactly the blocks already accumulated. On the last step
+    // the K buffer holds a stale tile: its scores and weights are never used.
+    auto step = [&](int t, f32x16& s_in, bf16x8(&p_in)[2], float& l_in, f32x16& s_out,
+                    bf16x8(&p_out)[2], float& l_out) {
+      const bool have_next = t + 1 < n_tiles;
+      // K(t+2) and V(t+1), loaded during the previous step, go to the buffers
+      // that tile t and tile t-1 freed; then the loads of K(t+3) and V(t+2) start.
+      kst.template store<Sh::kStrideK>(sK[t & 1], tid);
+      vst.template store<Sh::kStrideV>(sV[(t + 1) & 1], tid);
+      kst.load(Kh, kc.key0(), t + 3 < n_tiles ? kc.nvalid() : 0, tid);
+      vst.load(Vh, vc.key0(), t + 2 < n_tiles ? vc.nvalid() : 0, tid);
+      const uint16_t* kbuf = sK[(t + 1) & 1];
+      const uint16_t* vbuf = sV[t & 1];
+      const int nv_next = min(kBlockK, T - kt_next * kBlockK);
+      if (wave_active) {
+        f32x16 s2 = qk_block<D>(kbuf, qf, n, hf, 0);
+        bf16x8 p1[2];
+        float l1 = block_weights(s_in, c, m_ref * c, p1);
+        pv_block<D>(vbuf, p_in, lane, 0, o);
+        l_run += l_in;
+        interleave_half_step<D>();
+        if (__builtin_amdgcn_ballot_w64(l1 > lazy) != 0) rescale(s_in, p1, l1);
+        if (have_next && nv_next < kBlockK) mask_tail(s2, 0, hf, nv_next);
+
+        s_out = qk_block<D>(kbuf, qf, n, hf, 1);
+        l_out = block_weights(s2, c, m_ref * c, p_out);
+        pv_block<D>(vbuf, p1, lane, 1, o);
+        l_run += l1;
+        interleave_half_step<D>();
+        if (have_next) {
+          if (__builtin_amdgcn_ballot_w64(l_out > lazy) != 0) rescale(s2, p_out, l_out);
+          if (nv_next < kBlockK) mask_tail(s_out, 1, hf, nv_next);
+        }
+      }
       kc.advance(n_kept);
       vc.advance(n_kept);
+      if (++kt_next == tpf) kt_next = 0;
       __syncthreads();
     };
 
     int t = 0;
     for (; t + 1 < n_tiles; t += 2) {
-      step(t, sa, sb);
-      step(t + 1, sb, sa);
+      step(t, sa, pa, la, sb, pb, lb);
+      step(t + 1, sb, pb, lb, sa, pa, la);
     }
-    if (t < n_tiles) step(t, sa, sb);
+    if (t < n_tiles) step(t, sa, pa, la, sb, pb, lb);
   }
 
   // Epilogue: normalise, round to bf16 (RNE), store 4 consecutive d per access.
+  const float l_tot = pair_sum(l_run);
   if (qvalid) {
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     uint16_t* op = Oh + ((size_t)frame * T + qrow) * D;
 #pragma unroll
     for (int mb = 0; mb < Sh::kDBlocks; ++mb)

@@ -224,3 +224,19 @@ def test_full_size_sampled(name, form, g):
     assert_parity(got[b, h, s], ref, f"{name}-{form}-g{g}")
     # rows of frames that keep nothing do not exist in these masks; outputs are finite
     assert errors(got[:, :, :: max(1, w.T // 7)], np.zeros(1))["finite"]
+
+
+def test_last_query_block_with_idle_waves():
+    """At T = 3600 the last query block of each frame holds 16 rows, so three of its
+    four waves have no rows and only help load tiles. Those waves must not
+    overwrite a K buffer that the others still read; every row of the last blocks
+    of all frames and heads is compared, at a head count that fills the GPU."""
+    B, H, F, T, d = 1, 24, 3, 3600, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=21)
+    mask = om.tile_mask(F, 1, "col")
+    got = run_gpu(qb, kb, vb, mask, T, d ** -0.5)
+    rows = np.arange(T - 144, T)
+    for h in (0, 7, 23):
+        s = np.concatenate([f * T + rows for f in range(F)])
+        ref = oa.attention_rows(qb, kb, vb, mask, T, d ** -0.5, np.zeros_like(s), np.full_like(s, h), s)
+        assert_parity(got[0, h, s], ref, f"last-block-h{h}")
