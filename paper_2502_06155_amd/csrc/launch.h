@@ -5,8 +5,8 @@
 
 namespace ta {
 
-// Query rows per workgroup; each of the four waves owns 32 query rows.
-constexpr int kBlockQ = 128;
+// Query rows per workgroup; each of the four waves owns 64 query rows.
+constexpr int kBlockQ = 256;
 constexpr int kThreads = 256;
 
 struct FwdArgs {

@@ -77,7 +77,7 @@ int check_args(const void* q, const void* k, const void* v, void* out, int B, in
   const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
   const int64_t n_wg = (int64_t)B * H * F * nqb;
   if (n_wg * ta::kThreads > (int64_t)UINT32_MAX)
-    return fail(TA_ERR_BAD_SHAPE, "B * H * F * ceil(T / 128) workgroups exceed the grid limit");
+    return fail(TA_ERR_BAD_SHAPE, "B * H * F * ceil(T / 256) workgroups exceed the grid limit");
   if (!std::isfinite(scale)) return fail(TA_ERR_BAD_SCALE, "scale must be finite");
   for (const void* p : {q, k, v, (const void*)out})
     if (reinterpret_cast<uintptr_t>(p) % 16)

@@ -6,40 +6,40 @@
 // are skipped); the kernel walks a compact kept-frame list per query frame.
 //
 // Work decomposition
-//   One workgroup = 4 waves = 128 query rows of one (batch, head, query frame).
-//   Query blocks are frame aligned, so every row of a workgroup shares one kept
-//   list. Workgroup ids are remapped so that each XCD (8 per MI355X, each with
-//   its own L2) receives a contiguous run of (batch, head) problems, which keeps
-//   the K/V of the shared global frames resident in that XCD's L2.
+//   One workgroup = 4 waves = 256 query rows of one (batch, head, query frame);
+//   each wave owns 64 rows as two 32-query column blocks. Query blocks are frame
+//   aligned, so every row of a workgroup shares one kept list. Workgroup ids are
+//   remapped so that each XCD (8 per MI355X, each with its own L2) receives a
+//   contiguous run of (batch, head) problems, which keeps the K/V of the shared
+//   global frames resident in that XCD's L2. Two workgroups share a CU, so each
+//   SIMD runs two waves: while one forms softmax weights on the vector ALUs the
+//   other keeps the matrix cores busy.
 //
 // Matrix-core layout (v_mfma_f32_32x32x16_bf16, wave64)
 //   A (32 x 16): lane l holds row l%32, k = 8*(l/32) .. +7
 //   B (16 x 32): lane l holds col l%32, k = 8*(l/32) .. +7
 //   C (32 x 32): lane l holds col l%32, rows 8*i + 4*(l/32) + j at index 4*i + j
-//   The kernel computes S^T = K * Q^T (A = K rows from LDS, B = this wave's 32
-//   queries held in registers), so each lane owns ONE query and 16 of every 32
-//   keys. The probabilities P^T then sit exactly where the B operand of
-//   O^T += V^T * P^T expects them, with the contraction index k of chunk ch
-//   mapped to keys 16ch + 4h + (0..3) and 16ch + 8 + 4h + (0..3) for lane half h.
+//   The kernel computes S^T = K * Q^T (A = K rows from LDS, B = the wave's queries
+//   held in registers), so each lane owns one query per column block and 16 of
+//   every 32 keys. The probabilities P^T then sit exactly where the B operand of
+//   O^T += V^T * P^T expects them, with the contraction index k of chunk ch mapped
+//   to keys 16ch + 4h + (0..3) and 16ch + 8 + 4h + (0..3) for lane half h. Every
+//   K and V^T fragment read from LDS feeds two MFMAs (both column blocks), which
+//   halves the LDS read traffic per matrix instruction.
 //   The V^T operand is read from the untransposed V tile with the LDS transpose
 //   load ds_read_b64_tr_b16: inside each 16-lane group, lane i receives element
 //   i%4 of the 8-byte rows read by lanes 4k + i/4 (k = 0..3), so when lane j reads
 //   V[key0 + j/4][d0 + 4(j%4) .. +3], lane i gets V[key0 .. key0+3][d0 + i].
 //
-// Pipeline (one barrier per 64-key tile t)
-//   Step t stores K(t+2) and V(t+1), loaded into registers during step t-1, into
-//   the LDS buffers that tiles t and t-1 freed, and starts the global loads of
-//   K(t+3) and V(t+2), which have a whole step to arrive. It then runs in two
-//   halves over 32-key blocks: QK^T of a block of tile t+1, the weights of the
-//   previous block and PV of the one before, three independent pieces whose
-//   MFMAs and VALU work interleave. K and V each have two LDS buffers; K runs one
-//   tile ahead of V.
+// Tiles (64 keys) move from global memory straight into LDS with buffer loads
+// that write LDS (no register staging). K and V each have two LDS buffers: while
+// tile t is consumed, tile t+1 lands in the other pair; one barrier per tile.
 //
 // Online softmax (fp32, base 2): weights are exp2(c * (s - m_ref)) with
 // c = |scale| * log2(e) and m_ref an exponent reference per query that only
-// moves when needed. The first tile sets m_ref to its row max. After that the
-// weights are formed directly; if any lane's sum of weights in a tile exceeds
-// 2^kLazyLog2 (so some weight may have grown past it), that tile is redone with
+// moves when needed. Weights are formed directly; if any lane's sum of weights
+// in a 32-key block exceeds 2^kLazyLog2 (so some weight may have grown past it;
+// at the first block m_ref = -inf makes them infinite or NaN), the block is redone with
 // m_ref raised to the running max and O^T and l rescaled. Weights up to
 // 2^kLazyLog2 are as exact in fp32 and bf16 as weights up to 1, so the result is
 // the same softmax; only the reference of the exponentials moves less often. The
@@ -60,6 +60,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -68,27 +69,49 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kWaves = kThreads / 64;
-constexpr int kWaveQ = 32;   // query rows per wave: the N side of the 32x32 MFMA
+constexpr int kWaveQ = 64;   // query rows per wave: two 32-query column blocks
 constexpr int kBlockK = 64;  // keys per K/V tile staged in LDS
 constexpr float kLazyLog2 = 10.f;
 static_assert(kWaves * kWaveQ == kBlockQ, "workgroup rows");
 
 template <int D>
 struct Shape {
-  // LDS row strides (bf16). K rows are read 16 bytes per lane, 16 rows at a time:
-  // D + 8 spreads those rows over all 64 banks. V rows are read 8 bytes per lane by
-  // the transpose load, 4 rows x 64 bytes at a time: a stride of 48 or 16 banks
-  // (mod 64) keeps those four rows apart.
-  static constexpr int kStrideK = D + 8;
-  static constexpr int kStrideV = (D % 64 == 32) ? D : D + 32;
   static constexpr int kChunks = D / 16;   // 16-wide slices of the QK^T contraction
   static constexpr int kDBlocks = D / 32;  // 32-row blocks of O^T
   static constexpr int kPieces = D / 8;    // 16-byte pieces per K/V row
-  static constexpr int kPiecesPerThread = kBlockK * kPieces / kThreads;
-  static_assert(kBlockK * kPieces % kThreads == 0, "whole pieces per thread");
-  static constexpr int kSizeK = kBlockK * kStrideK;
-  static constexpr int kSizeV = kBlockK * kStrideV;
+  static constexpr int kTileElems = kBlockK * D;
+  // 16-byte direct loads per wave to fill one K or V tile (one load = 64 pieces).
+  static constexpr int kLoadsPerWave = kBlockK * kPieces / 64 / kWaves;
+  static_assert(kBlockK * kPieces == 64 * kWaves * kLoadsPerWave, "whole loads per wave");
 };
+
+// LDS tile layouts. A tile is kBlockK rows (keys) of D bf16, stored as rows of
+// kPieces 16-byte pieces with the pieces of each row permuted by an XOR, so that
+// the MFMA operand reads hit distinct banks:
+//   K (read 16 bytes per lane, 16 consecutive rows per access): piece p of row r
+//     sits at p ^ ksw(r), which spreads those 16 rows over all 64 banks;
+//   V (read 8 bytes per lane by the transpose load, 4 consecutive rows x 64 bytes
+//     per access): the 64-byte quads of row r are permuted by vsw(r), which puts
+//     those 4 rows in 4 different 64-byte bank groups.
+// Both XORs keep every aligned group of four pieces together, so one direct load
+// (64 lanes x 16 bytes into 1 KB of LDS) reads 1 KB of contiguous global memory.
+template <int D>
+__device__ __forceinline__ int ksw(int r) {
+  if constexpr (D == 64) return (r >> 1) & 7;
+  else if constexpr (D == 96) return (r >> 2) & 3;
+  else return r & 15;
+}
+template <int D>
+__device__ __forceinline__ int vsw(int r) {
+  if constexpr (D == 64) return ((r >> 1) & 1) << 2;
+  else if constexpr (D == 96) return 0;
+  else return (r & 3) << 2;
+}
+// Element offset in LDS of piece p (8 bf16) of row r.
+template <int D>
+__device__ __forceinline__ int k_slot(int r, int p) { return (r * (D / 8) + (p ^ ksw<D>(r))) * 8; }
+template <int D>
+__device__ __forceinline__ int v_slot(int r, int p) { return (r * (D / 8) + (p ^ vsw<D>(r))) * 8; }
 
 // Workgroup id -> logical work index such that the ids the hardware sends to
 // XCD x (those with id % 8 == x) cover one contiguous logical range.
@@ -134,18 +157,6 @@ struct TileCursor {
   __device__ __forceinline__ int nvalid() const { return min(kBlockK, T - kt * kBlockK); }
 };
 
-// Buffer resource over the valid rows of one tile: loads past nvalid rows return
-// zero (hardware range check), so tiles never read beyond their frame.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* base, int nvalid,
-                                                            int d) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0,
-                                           nvalid * d * 2, 0x00020000);
-}
-
-__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
-}
-
 // Both halves of the wave see max/sum over lanes l and l^32 (v_permlane32_swap
 // hands each lane its partner's value).
 __device__ __forceinline__ float pair_max(float x) {
@@ -159,38 +170,80 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
-// Register staging of one 64-key K or V tile: the tile is kBlockK * D contiguous
-// bf16 in global memory, cut into 16-byte pieces; thread tid moves pieces
-// tid, tid + 256, ... into LDS rows of the given stride.
-template <int D>
-struct Stage {
-  u32x4 r[Shape<D>::kPiecesPerThread];
-  __device__ __forceinline__ void load(const uint16_t* Xh, size_t key0, int nvalid, int tid) {
-    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(Xh + key0 * D, nvalid, D);
+// Buffer resource words (raw buffer, no stride) over `bytes` bytes at `base`;
+// loads past the end return zero, which keeps tile loads inside their frame.
+__device__ __forceinline__ i32x4 buffer_words(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xffffu), (int)bytes, 0x00020000};
+}
+
+// One 16-byte-per-lane buffer load written straight to LDS: lane L's 16 bytes
+// from byte offset voff land at LDS byte address lds + 16 L. Issued as inline
+// assembly so that the compiler does not order every later LDS read behind it;
+// completion is awaited explicitly with wait_tile_loads() before the barrier
+// that publishes the tile.
+__device__ __forceinline__ void load_to_lds(i32x4 rsrc, uint32_t lds, int voff) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds"
+      :
+      : "s"(lds), "v"(voff), "s"(rsrc)
+      : "memory", "m0");
+}
+
+// Waits until every buffer load of this wave, including those writing LDS, is done.
+__device__ __forceinline__ void wait_tile_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)p));
+}
+
+// Direct global -> LDS loads of one 64-key K or V tile (kBlockK * D contiguous bf16
+// in global memory). Load j of wave w fills LDS pieces [64 i, 64 i + 64) with
+// i = w + kWaves * j; lane L fills piece 64 i + L, which the layout maps back to
+// row r and source piece p. The source byte offsets depend only on the lane, so
+// they are computed once.
+template <int D, bool IS_K>
+struct TileLoader {
+  int off[Shape<D>::kLoadsPerWave];  // source byte offset within the tile, per load
+  __device__ __forceinline__ void init(int wave, int lane) {
 #pragma unroll
-    for (int i = 0; i < Shape<D>::kPiecesPerThread; ++i)
-      r[i] = buf_load16(rs, (tid + i * kThreads) * 16);
-  }
-  template <int STRIDE>
-  __device__ __forceinline__ void store(uint16_t* s, int tid) const {
-#pragma unroll
-    for (int i = 0; i < Shape<D>::kPiecesPerThread; ++i) {
-      const int idx = tid + i * kThreads;
-      const int row = idx / Shape<D>::kPieces, c8 = idx % Shape<D>::kPieces;
-      *reinterpret_cast<u32x4*>(s + row * STRIDE + 8 * c8) = r[i];
+    for (int j = 0; j < Shape<D>::kLoadsPerWave; ++j) {
+      const int q = 64 * (wave + kWaves * j) + lane;
+      const int r = q / Shape<D>::kPieces, ps = q % Shape<D>::kPieces;
+      const int p = ps ^ (IS_K ? ksw<D>(r) : vsw<D>(r));
+      off[j] = (r * D + 8 * p) * 2;
     }
+  }
+  // Rows past nvalid read as zeros (buffer range check).
+  __device__ __forceinline__ void load(const uint16_t* Xh, size_t key0, int nvalid,
+                                       const uint16_t* lds, int wave) const {
+    const i32x4 rs = buffer_words(Xh + key0 * D, (uint32_t)(nvalid * D * 2));
+    const uint32_t base = lds_addr(lds);
+#pragma unroll
+    for (int j = 0; j < Shape<D>::kLoadsPerWave; ++j)
+      load_to_lds(rs, __builtin_amdgcn_readfirstlane(base + 1024u * (uint32_t)(wave + kWaves * j)),
+                  off[j]);
   }
 };
 
-// S^T of 32-key block kb of a K tile (32 keys x 32 queries), raw logits.
+// S^T of 32-key block kb of a K tile for both 32-query column blocks of the wave
+// (32 keys x 32 queries each), raw logits. Each K fragment feeds two MFMAs.
 template <int D>
-__device__ __forceinline__ f32x16 qk_block(const uint16_t* sK, const bf16x8 (&qf)[D / 16], int n,
-                                           int hf, int kb) {
-  const uint16_t* row = sK + (kb * 32 + n) * Shape<D>::kStrideK + 8 * hf;
-  f32x16 s = mfma32(as_bf16x8(load16(row)), qf[0], f32x16{});
+__device__ __forceinline__ void qk_block(const uint16_t* sK, const bf16x8 (&qf)[2][D / 16], int n,
+                                         int hf, int kb, f32x16 (&s)[2]) {
+  const int r = kb * 32 + n;
+  const bf16x8 a0 = as_bf16x8(load16(sK + k_slot<D>(r, hf)));
+  s[0] = mfma32(a0, qf[0][0], f32x16{});
+  s[1] = mfma32(a0, qf[1][0], f32x16{});
 #pragma unroll
-  for (int cc = 1; cc < D / 16; ++cc) s = mfma32(as_bf16x8(load16(row + 16 * cc)), qf[cc], s);
-  return s;
+  for (int cc = 1; cc < D / 16; ++cc) {
+    const bf16x8 a = as_bf16x8(load16(sK + k_slot<D>(r, 2 * cc + hf)));
+    s[0] = mfma32(a, qf[0][cc], s[0]);
+    s[1] = mfma32(a, qf[1][cc], s[1]);
+  }
 }
 
 // Keys of block kb past the frame end get -inf: no part in the max, weight 0.
@@ -208,23 +261,29 @@ __device__ __forceinline__ void mask_tail(f32x16& s, int kb, int hf, int nvalid)
 template <int D>
 __device__ __forceinline__ bf16x8 vt_frag(const uint16_t* sV, int lane, int mb, int ch) {
   const int g = lane >> 4, j = lane & 15;
-  const uint16_t* p =
-      sV + (16 * ch + 4 * (g >> 1) + (j >> 2)) * Shape<D>::kStrideV + 32 * mb + 16 * (g & 1) + 4 * (j & 3);
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
-  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * Shape<D>::kStrideV));
+  const int r = 16 * ch + 4 * (g >> 1) + (j >> 2);       // key row (and r + 8)
+  const int pc = 4 * mb + 2 * (g & 1) + ((j >> 1) & 1);  // 16-byte piece holding d0
+  const int e = 4 * (j & 1);                             // d0's offset in that piece
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sV + v_slot<D>(r, pc) + e));
+  const i16x4 hi =
+      __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sV + v_slot<D>(r + 8, pc) + e));
   const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
   return as_bf16x8(u32x4{a[0], a[1], b[0], b[1]});
 }
 
-// O^T (d x 32 queries) += V^T * P^T over 32-key block kb (key chunks 2kb, 2kb+1).
+// O^T (d x 32 queries, both column blocks) += V^T * P^T over 32-key block kb (key
+// chunks 2kb, 2kb+1). Each V^T fragment feeds two MFMAs.
 template <int D>
-__device__ __forceinline__ void pv_block(const uint16_t* sV, const bf16x8 (&p)[2], int lane, int kb,
-                                         f32x16 (&o)[D / 32]) {
+__device__ __forceinline__ void pv_block(const uint16_t* sV, const bf16x8 (&p)[2][2], int lane,
+                                         int kb, f32x16 (&o)[2][D / 32]) {
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb)
-      o[mb] = mfma32(vt_frag<D>(sV, lane, mb, 2 * kb + c2), p[c2], o[mb]);
+    for (int mb = 0; mb < D / 32; ++mb) {
+      const bf16x8 a = vt_frag<D>(sV, lane, mb, 2 * kb + c2);
+      o[0][mb] = mfma32(a, p[0][c2], o[0][mb]);
+      o[1][mb] = mfma32(a, p[1][c2], o[1][mb]);
+    }
 }
 
 // This lane's max over its 16 scores of a block (-inf keys included).
@@ -256,24 +315,6 @@ __device__ __forceinline__ float block_weights(const f32x16& s, float c, float m
   return ls;
 }
 
-// Scheduling hint for one half step: D/16 LDS reads and D/16 MFMAs of QK^T,
-// D/16 transposed-read pairs and D/16 MFMAs of PV, and the weights of one block
-// (about 50 VALU instructions). A few LDS reads go first, then each MFMA is
-// followed by a slice of the VALU work and the next LDS reads, so the vector
-// ALUs work while each MFMA runs.
-template <int D>
-__device__ __forceinline__ void interleave_half_step() {
-  constexpr int kMfma = 2 * (D / 16);
-  constexpr int kValu = 52 / kMfma + 1;
-  __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);  // DS read
-#pragma unroll
-  for (int i = 0; i < kMfma; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);      // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x002, kValu, 0);  // VALU
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);      // DS read
-  }
-}
-
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
@@ -282,8 +323,8 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const int32_t* __restrict__ order, int F, int T, int nqb, uint32_t n_wg, float c,
     uint32_t qflip, uint32_t qmask) {
   using Sh = Shape<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][Sh::kSizeK];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][Sh::kSizeV];
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
 
   const uint32_t work = xcd_remap(blockIdx.x, n_wg);
   const uint32_t per_bh = (uint32_t)F * (uint32_t)nqb;
@@ -299,30 +340,36 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   uint16_t* Oh = O + bh * head_elems;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hf = lane >> 5;
 
-  // This lane's query row (within its frame) and its Q^T B-operand slices.
-  const int qrow = qb * kBlockQ + wave * kWaveQ + n;
-  const bool qvalid = qrow < T;
-  // Waves whose 32 rows all lie past the frame end only help stage tiles.
+  // This lane's two query rows (within the frame), one per 32-query column block,
+  // and their Q^T B-operand slices.
+  const int qrow0 = qb * kBlockQ + wave * kWaveQ + n;
+  // Waves whose rows all lie past the frame end only help load tiles.
   const bool wave_active = qb * kBlockQ + wave * kWaveQ < T;
-  bf16x8 qf[Sh::kChunks];
-  {
+  bf16x8 qf[2][Sh::kChunks];
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs) {
+    const int qrow = qrow0 + 32 * qs;
     const uint16_t* qp = Qh + ((size_t)frame * T + qrow) * D + 8 * hf;
 #pragma unroll
     for (int cc = 0; cc < Sh::kChunks; ++cc) {
       u32x4 x = {0u, 0u, 0u, 0u};
-      if (qvalid) x = (load16(qp + 16 * cc) & qmask) ^ qflip;
-      qf[cc] = as_bf16x8(x);
+      if (qrow < T) x = (load16(qp + 16 * cc) & qmask) ^ qflip;
+      qf[qs][cc] = as_bf16x8(x);
     }
   }
 
-  f32x16 o[Sh::kDBlocks];
+  f32x16 o[2][Sh::kDBlocks];
 #pragma unroll
-  for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[mb] = f32x16{};
-  float m_ref = -INFINITY;  // exponent reference (raw logit units) of this lane's query
-  float l_run = 0.f;        // this lane's part of the running sum of weights
+  for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+    for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[qs][mb] = f32x16{};
+  // Per column block: exponent reference (raw logit units) of this lane's query
+  // and this lane's part of the running sum of weights.
+  float m_ref[2] = {-INFINITY, -INFINITY};
+  float l_run[2] = {0.f, 0.f};
   const float lazy = exp2f(kLazyLog2);
 
   const int kbeg = row_ptr[frame];
@@ -331,129 +378,87 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   const int n_tiles = n_kept * tpf;
 
   if (n_tiles > 0) {
-    Stage<D> kst, vst;
-    // Prologue: K(0), V(0) and K(1) into LDS, scores of tile 0, then the loads of
-    // K(2) and V(1), which step 0 stores.
-    TileCursor kc, vc;
-    kc.start(cols + kbeg, tpf, T);
-    kst.load(Kh, kc.key0(), kc.nvalid(), tid);
-    vst.load(Vh, kc.key0(), kc.nvalid(), tid);
-    const int nv0 = kc.nvalid();
-    kst.template store<Sh::kStrideK>(sK[0], tid);
-    vst.template store<Sh::kStrideV>(sV[0], tid);
-    kc.advance(n_kept);
-    vc = kc;  // tile 1
-    if (n_tiles > 1) {
-      kst.load(Kh, kc.key0(), kc.nvalid(), tid);
-      kst.template store<Sh::kStrideK>(sK[1], tid);
-    }
-    kc.advance(n_kept);  // tile 2
+    TileLoader<D, true> kl;
+    TileLoader<D, false> vl;
+    kl.init(wave, lane);
+    vl.init(wave, lane);
+    TileCursor cur, nxt;  // tile t (being consumed) and tile t+1 (being loaded)
+    cur.start(cols + kbeg, tpf, T);
+    kl.load(Kh, cur.key0(), cur.nvalid(), sK[0], wave);
+    vl.load(Vh, cur.key0(), cur.nvalid(), sV[0], wave);
+    nxt = cur;
+    nxt.advance(n_kept);
+    wait_tile_loads();
     __syncthreads();
 
-    // Carried from one step to the next: the scores of the second block of tile
-    // t (sa/sb) and the weights and their lane sum of its first block (pa/pb, la/lb).
-    f32x16 sa, sb;
-    bf16x8 pa[2], pb[2];
-    float la = 0.f, lb = 0.f;
-    if (wave_active) {
-      f32x16 s0 = qk_block<D>(sK[0], qf, n, hf, 0);
-      sa = qk_block<D>(sK[0], qf, n, hf, 1);
-      if (nv0 < kBlockK) {
-        mask_tail(s0, 0, hf, nv0);
-        mask_tail(sa, 1, hf, nv0);
+    for (int t = 0; t < n_tiles; ++t) {
+      const int buf = t & 1;
+      // Tile t+1 lands in the buffers tile t-1 freed (all waves passed the last
+      // barrier) while tile t is consumed.
+      if (t + 1 < n_tiles) {
+        kl.load(Kh, nxt.key0(), nxt.nvalid(), sK[buf ^ 1], wave);
+        vl.load(Vh, nxt.key0(), nxt.nvalid(), sV[buf ^ 1], wave);
       }
-      // The first tile sets the exponent reference.
-      m_ref = pair_max(fmaxf(block_max(s0), block_max(sa)));
-      la = block_weights(s0, c, m_ref * c, pa);
-    }
-    // Tiles that do not exist are loaded with an empty range (all zeros).
-    kst.load(Kh, kc.key0(), n_tiles > 2 ? kc.nvalid() : 0, tid);
-    vst.load(Vh, vc.key0(), n_tiles > 1 ? vc.nvalid() : 0, tid);
-    kc.advance(n_kept);  // tile 3
-    vc.advance(n_kept);  // tile 2
-    int kt_next = tpf > 1 ? 1 : 0;  // index within its frame of tile t + 1
-    // Step 0 overwrites K(0)'s buffer with K(2); every wave must be done reading it.
-    __syncthreads();
-
-    // Raise the exponent reference to cover block s, rescale what is accumulated
-    // so far, and redo the block's weights.
-    auto rescale = [&](const f32x16& s_blk, bf16x8(&p)[2], float& l) {
-      const float m_new = fmaxf(m_ref, pair_max(block_max(s_blk)));
-      const float alpha = fast_exp2((m_ref - m_new) * c);
-      l_run *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[mb] *= alpha;
-      m_ref = m_new;
-      l = block_weights(s_blk, c, m_ref * c, p);
-    };
-
-    // Step t, in two halves over 32-key blocks b = 2t, 2t+1:
-    //   half 0: QK^T of block 2t+2 (tile t+1), weights of block 2t+1, PV of block 2t
-    //   half 1: QK^T of block 2t+3 (tile t+1), weights of block 2t+2, PV of block 2t+1
-    // The three parts of a half are independent, so their MFMAs and VALU work
-    // interleave. Block b's weights are checked before its PV; a rescale at that
-    // point multiplies exactly the blocks already accumulated. On the last step
-    // the K buffer holds a stale tile: its scores and weights are never used.
-    auto step = [&](int t, f32x16& s_in, bf16x8(&p_in)[2], float& l_in, f32x16& s_out,
-                    bf16x8(&p_out)[2], float& l_out) {
-      const bool have_next = t + 1 < n_tiles;
-      // K(t+2) and V(t+1), loaded during the previous step, go to the buffers
-      // that tile t and tile t-1 freed; then the loads of K(t+3) and V(t+2) start.
-      kst.template store<Sh::kStrideK>(sK[t & 1], tid);
-      vst.template store<Sh::kStrideV>(sV[(t + 1) & 1], tid);
-      kst.load(Kh, kc.key0(), t + 3 < n_tiles ? kc.nvalid() : 0, tid);
-      vst.load(Vh, vc.key0(), t + 2 < n_tiles ? vc.nvalid() : 0, tid);
-      const uint16_t* kbuf = sK[(t + 1) & 1];
-      const uint16_t* vbuf = sV[t & 1];
-      const int nv_next = min(kBlockK, T - kt_next * kBlockK);
+      const int nvalid = cur.nvalid();
       if (wave_active) {
-        f32x16 s2 = qk_block<D>(kbuf, qf, n, hf, 0);
-        bf16x8 p1[2];
-        float l1 = block_weights(s_in, c, m_ref * c, p1);
-        pv_block<D>(vbuf, p_in, lane, 0, o);
-        l_run += l_in;
-        interleave_half_step<D>();
-        if (__builtin_amdgcn_ballot_w64(l1 > lazy) != 0) rescale(s_in, p1, l1);
-        if (have_next && nv_next < kBlockK) mask_tail(s2, 0, hf, nv_next);
-
-        s_out = qk_block<D>(kbuf, qf, n, hf, 1);
-        l_out = block_weights(s2, c, m_ref * c, p_out);
-        pv_block<D>(vbuf, p1, lane, 1, o);
-        l_run += l1;
-        interleave_half_step<D>();
-        if (have_next) {
-          if (__builtin_amdgcn_ballot_w64(l_out > lazy) != 0) rescale(s2, p_out, l_out);
-          if (nv_next < kBlockK) mask_tail(s_out, 1, hf, nv_next);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          f32x16 s[2];
+          qk_block<D>(sK[buf], qf, n, hf, kb, s);
+          if (nvalid < kBlockK) {
+            mask_tail(s[0], kb, hf, nvalid);
+            mask_tail(s[1], kb, hf, nvalid);
+          }
+          bf16x8 p[2][2];
+          float ls[2];
+#pragma unroll
+          for (int qs = 0; qs < 2; ++qs) ls[qs] = block_weights(s[qs], c, m_ref[qs] * c, p[qs]);
+          // Written so that NaN also takes the rescale: at the first block
+          // m_ref = -inf turns masked keys into NaN weights.
+          if (__builtin_amdgcn_ballot_w64(!(ls[0] <= lazy && ls[1] <= lazy)) != 0) {
+            // Raise the references to cover this block, rescale what is
+            // accumulated so far, and redo the block's weights.
+#pragma unroll
+            for (int qs = 0; qs < 2; ++qs) {
+              const float m_new = fmaxf(m_ref[qs], pair_max(block_max(s[qs])));
+              const float alpha = fast_exp2((m_ref[qs] - m_new) * c);
+              l_run[qs] *= alpha;
+#pragma unroll
+              for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[qs][mb] *= alpha;
+              m_ref[qs] = m_new;
+              ls[qs] = block_weights(s[qs], c, m_new * c, p[qs]);
+            }
+          }
+          l_run[0] += ls[0];
+          l_run[1] += ls[1];
+          pv_block<D>(sV[buf], p, lane, kb, o);
         }
       }
-      kc.advance(n_kept);
-      vc.advance(n_kept);
-      if (++kt_next == tpf) kt_next = 0;
+      cur = nxt;
+      nxt.advance(n_kept);
+      wait_tile_loads();
       __syncthreads();
-    };
-
-    int t = 0;
-    for (; t + 1 < n_tiles; t += 2) {
-      step(t, sa, pa, la, sb, pb, lb);
-      step(t + 1, sb, pb, lb, sa, pa, la);
     }
-    if (t < n_tiles) step(t, sa, pa, la, sb, pb, lb);
   }
 
   // Epilogue: normalise, round to bf16 (RNE), store 4 consecutive d per access.
-  const float l_tot = pair_sum(l_run);
-  if (qvalid) {
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    uint16_t* op = Oh + ((size_t)frame * T + qrow) * D;
 #pragma unroll
-    for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+  for (int qs = 0; qs < 2; ++qs) {
+    const float l_tot = pair_sum(l_run[qs]);
+    const int qrow = qrow0 + 32 * qs;
+    if (qrow < T) {
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      uint16_t* op = Oh + ((size_t)frame * T + qrow) * D;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f32x4 x = {o[mb][4 * i + 0] * inv, o[mb][4 * i + 1] * inv, o[mb][4 * i + 2] * inv,
-                   o[mb][4 * i + 3] * inv};
-        const bf16x4 y = __builtin_convertvector(x, bf16x4);
-        *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
-      }
+      for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
+                     o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
+          const bf16x4 y = __builtin_convertvector(x, bf16x4);
+          *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
+        }
+    }
   }
 }
 
