@@ -229,18 +229,47 @@ struct TileLoader {
   }
 };
 
+// Per-lane LDS element offsets of this lane's K fragment pieces for 32-key block
+// 0 of a tile (row n of the block, piece 2 cc + h of each 16-wide chunk cc); the
+// swizzle of a row depends only on n, so block kb adds kb * 32 * D.
+template <int D>
+struct KAddr {
+  int at[D / 16];
+  __device__ __forceinline__ void init(int n, int hf) {
+#pragma unroll
+    for (int cc = 0; cc < D / 16; ++cc) at[cc] = k_slot<D>(n, 2 * cc + hf);
+  }
+};
+
+// Per-lane LDS element offsets of this lane's transposed V reads for key chunk 0
+// of a tile, one per 32-row d-block: lane l (group g = l/16, j = l%16) reads
+// V[4(g/2) + j/4][32mb + 16(g%2) + 4(j%4) .. +3]. Chunk ch adds 16 ch * D and the
+// second read (keys + 8) adds 8 * D: the swizzle of a row depends only on its
+// low two bits, which those steps do not change.
+template <int D>
+struct VAddr {
+  int at[D / 32];
+  __device__ __forceinline__ void init(int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const int r = 4 * (g >> 1) + (j >> 2);
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb)
+      at[mb] = v_slot<D>(r, 4 * mb + 2 * (g & 1) + ((j >> 1) & 1)) + 4 * (j & 1);
+  }
+};
+
 // S^T of 32-key block kb of a K tile for both 32-query column blocks of the wave
 // (32 keys x 32 queries each), raw logits. Each K fragment feeds two MFMAs.
 template <int D>
-__device__ __forceinline__ void qk_block(const uint16_t* sK, const bf16x8 (&qf)[2][D / 16], int n,
-                                         int hf, int kb, f32x16 (&s)[2]) {
-  const int r = kb * 32 + n;
-  const bf16x8 a0 = as_bf16x8(load16(sK + k_slot<D>(r, hf)));
+__device__ __forceinline__ void qk_block(const uint16_t* sK, const bf16x8 (&qf)[2][D / 16],
+                                         const KAddr<D>& ka, int kb, f32x16 (&s)[2]) {
+  const uint16_t* base = sK + kb * 32 * D;
+  const bf16x8 a0 = as_bf16x8(load16(base + ka.at[0]));
   s[0] = mfma32(a0, qf[0][0], f32x16{});
   s[1] = mfma32(a0, qf[1][0], f32x16{});
 #pragma unroll
   for (int cc = 1; cc < D / 16; ++cc) {
-    const bf16x8 a = as_bf16x8(load16(sK + k_slot<D>(r, 2 * cc + hf)));
+    const bf16x8 a = as_bf16x8(load16(base + ka.at[cc]));
     s[0] = mfma32(a, qf[0][cc], s[0]);
     s[1] = mfma32(a, qf[1][cc], s[1]);
   }
@@ -256,17 +285,14 @@ __device__ __forceinline__ void mask_tail(f32x16& s, int kb, int hf, int nvalid)
 }
 
 // V^T fragment (32 d-rows x 16 keys, A-operand layout) for d-block mb and key
-// chunk ch, from a V tile stored row-major (key, d) in LDS. Lane l: group
-// g = l/16, j = l%16 reads V[16ch + 4(g/2) + j/4 (+8)][32mb + 16(g%2) + 4(j%4) ..].
+// chunk ch from the V tile: lane i of each 16-lane group receives
+// V[key0 .. key0+3][d0 + i] from each of the two transposed reads (keys and
+// keys + 8).
 template <int D>
-__device__ __forceinline__ bf16x8 vt_frag(const uint16_t* sV, int lane, int mb, int ch) {
-  const int g = lane >> 4, j = lane & 15;
-  const int r = 16 * ch + 4 * (g >> 1) + (j >> 2);       // key row (and r + 8)
-  const int pc = 4 * mb + 2 * (g & 1) + ((j >> 1) & 1);  // 16-byte piece holding d0
-  const int e = 4 * (j & 1);                             // d0's offset in that piece
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sV + v_slot<D>(r, pc) + e));
-  const i16x4 hi =
-      __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(sV + v_slot<D>(r + 8, pc) + e));
+__device__ __forceinline__ bf16x8 vt_frag(const uint16_t* sV, const VAddr<D>& va, int mb, int ch) {
+  const uint16_t* p = sV + 16 * ch * D + va.at[mb];
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 8 * D));
   const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
   return as_bf16x8(u32x4{a[0], a[1], b[0], b[1]});
 }
@@ -274,13 +300,13 @@ __device__ __forceinline__ bf16x8 vt_frag(const uint16_t* sV, int lane, int mb, 
 // O^T (d x 32 queries, both column blocks) += V^T * P^T over 32-key block kb (key
 // chunks 2kb, 2kb+1). Each V^T fragment feeds two MFMAs.
 template <int D>
-__device__ __forceinline__ void pv_block(const uint16_t* sV, const bf16x8 (&p)[2][2], int lane,
-                                         int kb, f32x16 (&o)[2][D / 32]) {
+__device__ __forceinline__ void pv_block(const uint16_t* sV, const bf16x8 (&p)[2][2],
+                                         const VAddr<D>& va, int kb, f32x16 (&o)[2][D / 32]) {
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
     for (int mb = 0; mb < D / 32; ++mb) {
-      const bf16x8 a = vt_frag<D>(sV, lane, mb, 2 * kb + c2);
+      const bf16x8 a = vt_frag<D>(sV, va, mb, 2 * kb + c2);
       o[0][mb] = mfma32(a, p[0][c2], o[0][mb]);
       o[1][mb] = mfma32(a, p[1][c2], o[1][mb]);
     }
@@ -313,6 +339,21 @@ __device__ __forceinline__ float block_weights(const f32x16& s, float c, float m
     }
   }
   return ls;
+}
+
+// Scheduling hint for a region holding N_MFMA matrix instructions (with their LDS
+// fragment reads) and about N_VALU vector instructions that do not depend on
+// them: each MFMA is followed by a share of the VALU work, so the vector ALUs
+// issue while the matrix core runs.
+template <int N_MFMA, int N_VALU>
+__device__ __forceinline__ void interleave_mfma_valu() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
+#pragma unroll
+  for (int i = 0; i < N_MFMA; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, (N_VALU + N_MFMA - 1) / N_MFMA, 0);  // VALU
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                        // DS read
+  }
 }
 
 template <int D>
@@ -382,6 +423,10 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     TileLoader<D, false> vl;
     kl.init(wave, lane);
     vl.init(wave, lane);
+    KAddr<D> ka;
+    VAddr<D> va;
+    ka.init(n, hf);
+    va.init(lane);
     TileCursor cur, nxt;  // tile t (being consumed) and tile t+1 (being loaded)
     cur.start(cols + kbeg, tpf, T);
     kl.load(Kh, cur.key0(), cur.nvalid(), sK[0], wave);
@@ -390,6 +435,28 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     nxt.advance(n_kept);
     wait_tile_loads();
     __syncthreads();
+
+    // The weights of a block are used only once every lane's sum of them is at
+    // most 2^kLazyLog2; otherwise (written so that NaN also qualifies: at the first
+    // block m_ref = -inf turns masked keys into NaN weights) the references are
+    // raised to cover the block, what is accumulated so far is rescaled, and the
+    // block's weights are redone. Then the block's sums join the running sums.
+    auto check_block = [&](const f32x16(&s)[2], bf16x8(&p)[2][2], float(&ls)[2]) {
+      if (__builtin_amdgcn_ballot_w64(!(ls[0] <= lazy && ls[1] <= lazy)) != 0) {
+#pragma unroll
+        for (int qs = 0; qs < 2; ++qs) {
+          const float m_new = fmaxf(m_ref[qs], pair_max(block_max(s[qs])));
+          const float alpha = fast_exp2((m_ref[qs] - m_new) * c);
+          l_run[qs] *= alpha;
+#pragma unroll
+          for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[qs][mb] *= alpha;
+          m_ref[qs] = m_new;
+          ls[qs] = block_weights(s[qs], c, m_new * c, p[qs]);
+        }
+      }
+      l_run[0] += ls[0];
+      l_run[1] += ls[1];
+    };
 
     for (int t = 0; t < n_tiles; ++t) {
       const int buf = t & 1;
@@ -401,38 +468,32 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
       }
       const int nvalid = cur.nvalid();
       if (wave_active) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          f32x16 s[2];
-          qk_block<D>(sK[buf], qf, n, hf, kb, s);
-          if (nvalid < kBlockK) {
-            mask_tail(s[0], kb, hf, nvalid);
-            mask_tail(s[1], kb, hf, nvalid);
-          }
-          bf16x8 p[2][2];
-          float ls[2];
-#pragma unroll
-          for (int qs = 0; qs < 2; ++qs) ls[qs] = block_weights(s[qs], c, m_ref[qs] * c, p[qs]);
-          // Written so that NaN also takes the rescale: at the first block
-          // m_ref = -inf turns masked keys into NaN weights.
-          if (__builtin_amdgcn_ballot_w64(!(ls[0] <= lazy && ls[1] <= lazy)) != 0) {
-            // Raise the references to cover this block, rescale what is
-            // accumulated so far, and redo the block's weights.
-#pragma unroll
-            for (int qs = 0; qs < 2; ++qs) {
-              const float m_new = fmaxf(m_ref[qs], pair_max(block_max(s[qs])));
-              const float alpha = fast_exp2((m_ref[qs] - m_new) * c);
-              l_run[qs] *= alpha;
-#pragma unroll
-              for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[qs][mb] *= alpha;
-              m_ref[qs] = m_new;
-              ls[qs] = block_weights(s[qs], c, m_new * c, p[qs]);
-            }
-          }
-          l_run[0] += ls[0];
-          l_run[1] += ls[1];
-          pv_block<D>(sV[buf], p, lane, kb, o);
+        // Within the tile: QK^T of block 1 runs on the matrix cores while the
+        // weights of block 0 form on the vector ALUs, then PV of block 0 while the
+        // weights of block 1 form, then PV of block 1.
+        f32x16 s0[2], s1[2];
+        bf16x8 p0[2][2], p1[2][2];
+        float l0[2], l1[2];
+        qk_block<D>(sK[buf], qf, ka, 0, s0);
+        if (nvalid < kBlockK) {
+          mask_tail(s0[0], 0, hf, nvalid);
+          mask_tail(s0[1], 0, hf, nvalid);
         }
+        qk_block<D>(sK[buf], qf, ka, 1, s1);
+#pragma unroll
+        for (int qs = 0; qs < 2; ++qs) l0[qs] = block_weights(s0[qs], c, m_ref[qs] * c, p0[qs]);
+        interleave_mfma_valu<2 * (D / 16), 48>();
+        check_block(s0, p0, l0);
+        if (nvalid < kBlockK) {
+          mask_tail(s1[0], 1, hf, nvalid);
+          mask_tail(s1[1], 1, hf, nvalid);
+        }
+        pv_block<D>(sV[buf], p0, va, 0, o);
+#pragma unroll
+        for (int qs = 0; qs < 2; ++qs) l1[qs] = block_weights(s1[qs], c, m_ref[qs] * c, p1[qs]);
+        interleave_mfma_valu<2 * (D / 16), 48>();
+        check_block(s1, p1, l1);
+        pv_block<D>(sV[buf], p1, va, 1, o);
       }
       cur = nxt;
       nxt.advance(n_kept);
