@@ -114,6 +114,28 @@ def cpu_baseline(w, qb, kb, vb, mask, budget_s: float):
     }
 
 
+def gemm_reference(torch, n: int = 16384, reps: int = 5):
+    """Dense bf16 GEMM (torch.matmul, i.e. the vendor BLAS) on N(0,1) data of the same
+    GPU: the matrix-core rate this chip sustains on random data under its power
+    limit, reported beside the published peak as context."""
+    g = torch.Generator(device="cuda").manual_seed(0)
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16, generator=g)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16, generator=g)
+    for _ in range(2):
+        a @ b
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return {"shape": f"{n}x{n}x{n} bf16 N(0,1), torch.matmul", "ms": ms,
+            "tflops": 2.0 * n ** 3 / (ms * 1e-3) / 1e12}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +148,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-gemm-ref", action="store_true")
     ap.add_argument("--profile-pass", action="store_true",
                     help="counter pass: sparse calls, then a plain copy of --copy-mib MiB "
                          "(the calibration kernel for HBM byte counters); no dense, no CPU")
@@ -134,6 +157,7 @@ def main():
     if args.profile_pass:
         args.no_dense = True
         args.no_cpu_baseline = True
+        args.no_gemm_ref = True
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the attention "
@@ -205,6 +229,11 @@ def main():
         log(f"[bench] dense: {dms:.3f} ms/call, {extra['dense_tflops']:.1f} TFLOP/s, "
             f"speedup {extra['speedup_vs_dense']:.2f}x of ideal {extra['ideal_speedup']:.2f}x")
 
+    gemm = None
+    if not args.no_gemm_ref:
+        gemm = gemm_reference(torch)
+        log(f"[bench] vendor bf16 GEMM on random data: {gemm['tflops']:.1f} TFLOP/s")
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, qb, kb, vb, mask, args.cpu_budget)
@@ -242,6 +271,7 @@ def main():
             "traffic": traffic_from_profile(),
         },
         "cpu_baseline": cpu,
+        "gemm_reference": gemm,
     }
     line.update(extra)
     print(json.dumps(line), flush=True)
