@@ -136,6 +136,61 @@ def gemm_reference(torch, n: int = 16384, reps: int = 5):
             "tflops": 2.0 * n ** 3 / (ms * 1e-3) / 1e12}
 
 
+# Every workload of the measurement plan: (workload, mask form, g). The dense control is
+# timed once per workload.
+ALL_CASES = [
+    ("tiny", "col", 1), ("tiny", "sym", 1),
+    ("29f", "col", 1), ("29f", "sym", 1),
+    ("93f", "col", 1), ("93f", "sym", 1),
+    ("sweep", "col", 1), ("sweep", "col", 2), ("sweep", "col", 4), ("sweep", "col", 8),
+    ("sweep", "sym", 2), ("sweep", "sym", 4), ("sweep", "sym", 8),
+    ("sp_share", "col", 1), ("sp_share", "sym", 1),
+    ("long", "col", 2), ("long", "sym", 2),
+]
+
+
+def run_all(args, torch, ta):
+    """Time every case of ALL_CASES and the dense control of each workload; print one
+    table row per case to stderr and return the rows."""
+    rows, cur, dense_ms = [], None, {}
+    order = []
+    for wname in dict.fromkeys(c[0] for c in ALL_CASES):
+        order += [c for c in ALL_CASES if c[0] == wname] + [(wname, "dense", 0)]
+    for name, form, g in order:
+        w = workloads.WORKLOADS[name]
+        if cur is None or cur[0] != name:
+            qb, kb, vb = workloads.make_workload_qkv(w)
+            dev = [torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda() for x in (qb, kb, vb)]
+            del qb, kb, vb
+            out = torch.empty_like(dev[0])
+            cur = (name, dev, out)
+        q, k, v = cur[1]
+        out = cur[2]
+        mask = ta.tile_attn_make_mask(w.F, g, form)
+        nnz = int(np.count_nonzero(mask))
+        stream = torch.cuda.current_stream()
+
+        def step():
+            ta.tile_attn_fwd(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), stream)
+
+        steps = max(3, min(args.steps, int(2000 / max(1.0, nnz))))
+        total, per = time_calls(step, steps, 2, torch)
+        ms = total / steps
+        tf = kept_flop(w, nnz) / (ms * 1e-3) / 1e12
+        if form == "dense":
+            dense_ms[name] = ms
+        row = {"workload": name, "form": form, "g": g, "nnz": nnz, "tiles": w.F * w.F, "ms": ms,
+               "tflops": tf, "pct_peak": 100.0 * tf / PEAK_BF16_TFLOPS}
+        rows.append(row)
+        log(f"[all] {name:8s} {form:5s} g={g} nnz {nnz:4d}/{w.F * w.F:<4d} {ms:9.3f} ms "
+            f"{tf:7.1f} TFLOP/s ({row['pct_peak']:.1f}% of peak)")
+    for row in rows:
+        if row["workload"] in dense_ms and row["form"] != "dense":
+            row["speedup_vs_dense"] = dense_ms[row["workload"]] / row["ms"]
+            row["ideal_speedup"] = row["tiles"] / row["nnz"]
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,6 +208,9 @@ def main():
                     help="counter pass: sparse calls, then a plain copy of --copy-mib MiB "
                          "(the calibration kernel for HBM byte counters); no dense, no CPU")
     ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--all", action="store_true",
+                    help="time every workload and mask of the measurement plan instead of the "
+                         "headline; prints one JSON line with a row per case")
     args = ap.parse_args()
     if args.profile_pass:
         args.no_dense = True
@@ -172,6 +230,12 @@ def main():
     if not torch.cuda.is_available():
         log("no GPU visible")
         sys.exit(1)
+
+    if args.all:
+        rows = run_all(args, torch, ta)
+        print(json.dumps({"metric": "per-case ms/call and TFLOP/s over kept tiles", "unit": "TFLOP/s",
+                          "n_gpus": 1, "dtype": "bf16", "data": "synthetic", "rows": rows}), flush=True)
+        return
 
     w = workloads.WORKLOADS[args.workload]
     g = w.g if args.g is None else args.g
