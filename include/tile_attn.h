@@ -29,9 +29,12 @@
  *     and nothing is enqueued. A HIP failure returns TA_ERR_HIP; the detail is in
  *     tile_attn_last_error().
  *   - Thread-safe. The first call for a given mask (per device) uploads its
- *     compact kept-tile list with a blocking allocation and copy; later calls
- *     with the same mask allocate nothing and do not synchronise, so a warmed-up
- *     call can be captured in a HIP graph.
+ *     work plan (tile_attn_plan) with a blocking allocation and copy. A mask
+ *     whose plan splits heavy query frames also needs a workspace for the
+ *     partial results, n_slots * B * H * T * (d + 1) * 4 bytes, held per
+ *     (device, stream) and grown (with a wait on that stream) when a call needs
+ *     more. Later calls that fit allocate nothing and do not synchronise, so a
+ *     warmed-up call can be captured in a HIP graph.
  */
 #ifndef TILE_ATTN_H
 #define TILE_ATTN_H
@@ -110,6 +113,27 @@ int tile_attn_make_mask(int F, int k, int form, uint8_t* mask_out);
  */
 int tile_attn_compact(const uint8_t* tile_mask, int F, int32_t* row_ptr,
                       uint16_t* cols, uint16_t* order, int* nnz);
+
+/*
+ * The work plan the kernels execute for a mask (host only, touches no GPU). Every
+ * query frame is one work item over its kept key frames, except that a frame
+ * keeping more than twice the mean number of kept frames per row (rounded up) is
+ * split into up to 32 items of about that mean size, whose partial results
+ * (slot >= 0) a merge pass combines by their log-sum-exp: one heavy row (the
+ * global query frames of the symmetric mask keep every frame) then no longer
+ * sets the critical path of the launch. The pieces of a split frame cover its
+ * kept list contiguously and in order. tile_attn_fwd falls back to the unsplit
+ * plan when the partial results would need more than 2 GiB.
+ *
+ * items: HOST int32[4 * cap]; item i is {query frame, first kept entry (index into
+ *   the row-after-row kept list of tile_attn_compact), number of kept entries,
+ *   slot or -1}, items ordered by descending kept count (ties keep frame order).
+ * n_items, n_slots: HOST ints receiving the item and partial-slot counts.
+ * Errors: TA_ERR_NULL_PTR, TA_ERR_BAD_SHAPE (F out of range, or cap < n_items; the
+ * counts are still written).
+ */
+int tile_attn_plan(const uint8_t* tile_mask, int F, int32_t* items, int cap, int* n_items,
+                   int* n_slots);
 
 /* Static text for a status code. */
 const char* tile_attn_status_string(int status);

@@ -15,4 +15,5 @@ from .api import (  # noqa: F401
     tile_attn_compact,
     tile_attn_fwd,
     tile_attn_make_mask,
+    tile_attn_plan,
 )

@@ -90,6 +90,20 @@ def tile_attn_compact(tile_mask):
     return row_ptr, cols[: nnz.value].copy(), order
 
 
+def tile_attn_plan(tile_mask):
+    """Work plan of a mask: (items int32[n, 4] = frame, first kept entry, count, slot;
+    number of partial slots)."""
+    m = np.asarray(tile_mask)
+    F = m.shape[0]
+    m = _mask_bytes(m, F)
+    cap = 33 * F
+    items = np.zeros(4 * cap, dtype=np.int32)
+    n_items, n_slots = ctypes.c_int(0), ctypes.c_int(0)
+    _check(lib.tile_attn_plan(m.ctypes.data, F, items.ctypes.data, cap, ctypes.byref(n_items),
+                              ctypes.byref(n_slots)), "tile_attn_plan")
+    return items[: 4 * n_items.value].reshape(-1, 4).copy(), n_slots.value
+
+
 def _shape_of(q, T: int):
     if q.dim() != 4:
         raise ValueError("expected [B, H, S, d] tensors")

@@ -15,15 +15,33 @@ struct FwdArgs {
   const uint16_t* v;
   uint16_t* out;
   int B, H, F, T, d;
-  const int32_t* row_ptr;  // device, F + 1
-  const int32_t* cols;     // device, nnz: kept key frames, row after row
-  const int32_t* order;    // device, F: dispatch order of query frames
-  float c;                 // > 0: |scale| * log2(e), logits in base-2 units
-  uint32_t qflip;          // 0x80008000 flips the sign of q (negative scale), else 0
-  uint32_t qmask;          // 0 zeroes q (scale 0: exactly uniform weights), else ~0
-  uint32_t n_wg;           // B * H * F * ceil(T / kBlockQ)
+  // Work items, 4 int32 each, in dispatch order: {query frame, first kept entry in
+  // cols, number of kept entries, partial slot or -1}. A query frame with many kept
+  // frames is split into several items (slots >= 0) whose partial results the merge
+  // kernel combines; every other frame is one item (slot -1) that writes out.
+  const int32_t* items;
+  const int32_t* cols;  // kept key frames, row after row
+  int n_items;
+  float* ws_o;          // partial O/l, fp32 [n_slots][B*H][T][d] (null if no slots)
+  float* ws_lse;        // partial base-2 log-sum-exp, fp32 [n_slots][B*H][T]
+  float c;              // > 0: |scale| * log2(e), logits in base-2 units
+  uint32_t qflip;       // 0x80008000 flips the sign of q (negative scale), else 0
+  uint32_t qmask;       // 0 zeroes q (scale 0: exactly uniform weights), else ~0
+  uint32_t n_wg;        // B * H * n_items * ceil(T / kBlockQ)
+};
+
+// Combines the partial results of split query frames: heavy holds 3 int32 per split
+// frame {query frame, first slot, number of slots}.
+struct MergeArgs {
+  const float* ws_o;
+  const float* ws_lse;
+  const int32_t* heavy;
+  int n_heavy;
+  int BH, F, T, d;
+  uint16_t* out;
 };
 
 hipError_t launch_tile_attn_fwd(const FwdArgs& a, hipStream_t stream);
+hipError_t launch_merge_partials(const MergeArgs& a, hipStream_t stream);
 
 }  // namespace ta

@@ -1,6 +1,8 @@
 // C-ABI entry points: argument checks, the k:(F-k) mask builder, compaction of
-// the frame mask into a kept-tile list, a per-device cache of that list, and
-// dispatch of the gfx950 kernel on the caller's stream.
+// the frame mask into a kept-tile list and a work plan (query frames with many
+// kept frames split into balanced pieces), a per-device cache of that plan, a
+// per-(device, stream) workspace for the partial results of split frames, and
+// dispatch of the gfx950 kernels on the caller's stream.
 #include "../../include/tile_attn.h"
 
 #include <hip/hip_runtime_api.h>
@@ -28,19 +30,6 @@ int fail(int status, const std::string& detail) {
   return status;
 }
 
-// Kept-tile list of one mask, resident on one device, in 32-bit words so the
-// kernels read it with scalar loads.
-struct DeviceKeptList {
-  void* buffer = nullptr;  // [row_ptr int32 F+1][order int32 F][cols int32 nnz]
-  const int32_t* row_ptr = nullptr;
-  const int32_t* order = nullptr;
-  const int32_t* cols = nullptr;
-  int nnz = 0;
-};
-
-std::mutex g_cache_mutex;
-std::map<std::pair<int, std::string>, DeviceKeptList> g_cache;
-
 void compact_host(const uint8_t* mask, int F, int32_t* row_ptr, uint16_t* cols,
                   uint16_t* order, int* nnz_out) {
   int nnz = 0;
@@ -60,6 +49,78 @@ void compact_host(const uint8_t* mask, int F, int32_t* row_ptr, uint16_t* cols,
   }
   *nnz_out = nnz;
 }
+
+// Work plan of one mask. Every query frame is one work item over its kept key
+// frames, except that a frame keeping more than twice the mean number of kept
+// frames per row (rounded up) is split into items of about that mean size: those
+// items write partial results (slot >= 0) that a merge pass combines. Splitting
+// keeps one heavy row (the global query frames of the symmetric mask keep every
+// frame) from setting the critical path while the other workgroups idle.
+struct WorkPlan {
+  std::vector<int32_t> items;  // 4 per item: frame, first kept entry, count, slot
+  std::vector<int32_t> cols;   // kept key frames, row after row
+  std::vector<int32_t> heavy;  // 3 per split frame: frame, first slot, slots
+  int n_slots = 0;
+};
+
+constexpr int kMaxChunksPerFrame = 32;
+
+WorkPlan plan_work(const uint8_t* mask, int F, bool allow_split) {
+  WorkPlan pl;
+  std::vector<int32_t> row_ptr(F + 1);
+  std::vector<uint16_t> cols((size_t)F * F + 1), order(F);
+  int nnz = 0;
+  compact_host(mask, F, row_ptr.data(), cols.data(), order.data(), &nnz);
+  pl.cols.assign(cols.begin(), cols.begin() + nnz);
+  if (pl.cols.empty()) pl.cols.push_back(0);
+  const int chunk = std::max(1, (nnz + F - 1) / F);  // mean kept frames per row, rounded up
+  struct Item { int frame, beg, cnt, slot; };
+  std::vector<Item> list;
+  for (int i = 0; i < F; ++i) {
+    const int beg = row_ptr[i], cnt = row_ptr[i + 1] - row_ptr[i];
+    int pieces = 1;
+    if (allow_split && cnt > 2 * chunk) pieces = std::min((cnt + chunk - 1) / chunk, kMaxChunksPerFrame);
+    if (pieces == 1) {
+      list.push_back({i, beg, cnt, -1});
+      continue;
+    }
+    pl.heavy.insert(pl.heavy.end(), {i, pl.n_slots, pieces});
+    for (int p = 0; p < pieces; ++p) {
+      const int b0 = beg + (int)((int64_t)cnt * p / pieces);
+      const int b1 = beg + (int)((int64_t)cnt * (p + 1) / pieces);
+      list.push_back({i, b0, b1 - b0, pl.n_slots++});
+    }
+  }
+  // Longest items first; ties keep frame and piece order.
+  std::stable_sort(list.begin(), list.end(),
+                   [](const Item& x, const Item& y) { return x.cnt > y.cnt; });
+  for (const Item& it : list) pl.items.insert(pl.items.end(), {it.frame, it.beg, it.cnt, it.slot});
+  return pl;
+}
+
+// A work plan resident on one device: [items][cols][heavy] in int32 words, read
+// by the kernels with scalar loads.
+struct DeviceWorkList {
+  void* buffer = nullptr;
+  const int32_t* items = nullptr;
+  const int32_t* cols = nullptr;
+  const int32_t* heavy = nullptr;
+  int n_items = 0, n_heavy = 0, n_slots = 0;
+};
+
+std::mutex g_cache_mutex;
+std::map<std::pair<int, std::string>, DeviceWorkList> g_cache;
+
+// Partial-result workspace of split frames, one per (device, stream) so that calls
+// on different streams never share it; grown on demand, kept until process exit.
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::map<std::pair<int, void*>, Workspace> g_workspaces;
+
+// Largest workspace a call may use; masks that would need more are not split.
+constexpr size_t kMaxWorkspaceBytes = size_t(2) << 30;
 
 bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
   auto x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
@@ -88,55 +149,87 @@ int check_args(const void* q, const void* k, const void* v, void* out, int B, in
   return TA_OK;
 }
 
-// Returns the device-resident kept list for `mask`, uploading it on first use.
-int kept_list_for(const uint8_t* mask, int F, const DeviceKeptList** out) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+// Returns the device-resident work list for `mask` (split or not), uploading it on
+// first use on the current device.
+int work_list_for(const uint8_t* mask, int F, bool allow_split, int dev,
+                  const DeviceWorkList** out) {
   std::string key(reinterpret_cast<const char*>(mask), (size_t)F * F);
+  key.push_back(allow_split ? 's' : 'u');
   std::lock_guard<std::mutex> lock(g_cache_mutex);
   auto it = g_cache.find({dev, key});
   if (it != g_cache.end()) {
     *out = &it->second;
     return TA_OK;
   }
-  std::vector<int32_t> row_ptr(F + 1);
-  std::vector<uint16_t> cols((size_t)F * F + 1), order(F);
-  int nnz = 0;
-  compact_host(mask, F, row_ptr.data(), cols.data(), order.data(), &nnz);
+  const WorkPlan pl = plan_work(mask, F, allow_split);
   std::vector<int32_t> words;
-  words.reserve((size_t)2 * F + 1 + std::max(nnz, 1));
-  words.insert(words.end(), row_ptr.begin(), row_ptr.end());
-  const size_t off_order = words.size();
-  words.insert(words.end(), order.begin(), order.end());
+  words.insert(words.end(), pl.items.begin(), pl.items.end());
   const size_t off_cols = words.size();
-  words.insert(words.end(), cols.begin(), cols.begin() + nnz);
-  if (nnz == 0) words.push_back(0);
+  words.insert(words.end(), pl.cols.begin(), pl.cols.end());
+  const size_t off_heavy = words.size();
+  words.insert(words.end(), pl.heavy.begin(), pl.heavy.end());
+  if (pl.heavy.empty()) words.push_back(0);
   const size_t total = words.size() * sizeof(int32_t);
   void* buf = nullptr;
-  e = hipMalloc(&buf, total);
+  hipError_t e = hipMalloc(&buf, total);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
   e = hipMemcpy(buf, words.data(), total, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(buf);
     return fail(TA_ERR_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
   }
-  DeviceKeptList entry;
+  DeviceWorkList entry;
   entry.buffer = buf;
-  entry.row_ptr = static_cast<const int32_t*>(buf);
-  entry.order = static_cast<const int32_t*>(buf) + off_order;
+  entry.items = static_cast<const int32_t*>(buf);
   entry.cols = static_cast<const int32_t*>(buf) + off_cols;
-  entry.nnz = nnz;
+  entry.heavy = static_cast<const int32_t*>(buf) + off_heavy;
+  entry.n_items = (int)(pl.items.size() / 4);
+  entry.n_heavy = (int)(pl.heavy.size() / 3);
+  entry.n_slots = pl.n_slots;
   auto res = g_cache.emplace(std::make_pair(dev, std::move(key)), entry);
   *out = &res.first->second;
   return TA_OK;
 }
 
+// Workspace of at least `bytes` for (dev, stream). Growing it waits for the
+// stream, whose earlier calls may still be using the old one.
+int workspace_for(int dev, void* stream, size_t bytes, void** out) {
+  std::lock_guard<std::mutex> lock(g_cache_mutex);
+  Workspace& ws = g_workspaces[{dev, stream}];
+  if (ws.bytes < bytes) {
+    hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipStreamSynchronize: ") + hipGetErrorString(e));
+    if (ws.ptr) (void)hipFree(ws.ptr);
+    ws.ptr = nullptr;
+    ws.bytes = 0;
+    e = hipMalloc(&ws.ptr, bytes);
+    if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
+    ws.bytes = bytes;
+  }
+  *out = ws.ptr;
+  return TA_OK;
+}
+
 int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F, int T,
             int d, const uint8_t* mask, float scale, void* stream) {
-  const DeviceKeptList* kl = nullptr;
-  int st = kept_list_for(mask, F, &kl);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
+  const DeviceWorkList* wl = nullptr;
+  int st = work_list_for(mask, F, true, dev, &wl);
   if (st != TA_OK) return st;
+  const size_t ws_bytes = (size_t)wl->n_slots * B * H * T * (d + 1) * sizeof(float);
+  const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
+  if (ws_bytes > kMaxWorkspaceBytes || (int64_t)B * H * wl->n_items * nqb > max_wg) {
+    st = work_list_for(mask, F, false, dev, &wl);  // the same frames, not split
+    if (st != TA_OK) return st;
+  }
+  void* ws = nullptr;
+  if (wl->n_slots > 0) {
+    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * H * T * (d + 1) * sizeof(float), &ws);
+    if (st != TA_OK) return st;
+  }
   ta::FwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -147,9 +240,11 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   a.F = F;
   a.T = T;
   a.d = d;
-  a.row_ptr = kl->row_ptr;
-  a.cols = kl->cols;
-  a.order = kl->order;
+  a.items = wl->items;
+  a.cols = wl->cols;
+  a.n_items = wl->n_items;
+  a.ws_o = static_cast<float*>(ws);
+  a.ws_lse = ws ? static_cast<float*>(ws) + (size_t)wl->n_slots * B * H * T * d : nullptr;
   // Logits are formed from |scale| (a negative scale flips the sign of q, which
   // is exact in bf16). scale == 0 zeroes q instead, so every logit is exactly 0
   // and the weights exactly uniform; c only has to stay positive.
@@ -162,9 +257,23 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
     a.qflip = std::signbit(scale) ? 0x80008000u : 0u;
     a.qmask = 0xFFFFFFFFu;
   }
-  a.n_wg = (uint32_t)((int64_t)B * H * F * ((T + ta::kBlockQ - 1) / ta::kBlockQ));
-  hipError_t e = ta::launch_tile_attn_fwd(a, static_cast<hipStream_t>(stream));
+  a.n_wg = (uint32_t)((int64_t)B * H * wl->n_items * nqb);
+  e = ta::launch_tile_attn_fwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  if (wl->n_heavy > 0) {
+    ta::MergeArgs m;
+    m.ws_o = a.ws_o;
+    m.ws_lse = a.ws_lse;
+    m.heavy = wl->heavy;
+    m.n_heavy = wl->n_heavy;
+    m.BH = B * H;
+    m.F = F;
+    m.T = T;
+    m.d = d;
+    m.out = a.out;
+    e = ta::launch_merge_partials(m, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
+  }
   g_last_error.clear();
   return TA_OK;
 }
@@ -201,6 +310,19 @@ int tile_attn_compact(const uint8_t* tile_mask, int F, int32_t* row_ptr, uint16_
     return fail(TA_ERR_NULL_PTR, "tile_mask, row_ptr, cols and nnz must be non-NULL");
   if (F < 1 || F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F must be in 1..TA_MAX_FRAMES");
   compact_host(tile_mask, F, row_ptr, cols, order, nnz);
+  return TA_OK;
+}
+
+int tile_attn_plan(const uint8_t* tile_mask, int F, int32_t* items, int cap, int* n_items,
+                   int* n_slots) {
+  if (!tile_mask || !items || !n_items || !n_slots)
+    return fail(TA_ERR_NULL_PTR, "tile_mask, items, n_items and n_slots must be non-NULL");
+  if (F < 1 || F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F must be in 1..TA_MAX_FRAMES");
+  const WorkPlan pl = plan_work(tile_mask, F, true);
+  *n_items = (int)(pl.items.size() / 4);
+  *n_slots = pl.n_slots;
+  if (cap < *n_items) return fail(TA_ERR_BAD_SHAPE, "cap is smaller than the number of items");
+  std::copy(pl.items.begin(), pl.items.end(), items);
   return TA_OK;
 }
 

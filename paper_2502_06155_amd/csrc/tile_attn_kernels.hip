@@ -360,18 +360,22 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-    const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ cols,
-    const int32_t* __restrict__ order, int F, int T, int nqb, uint32_t n_wg, float c,
-    uint32_t qflip, uint32_t qmask) {
+    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int F,
+    int T, int nqb, uint32_t n_wg, float* __restrict__ ws_o, float* __restrict__ ws_lse,
+    float c, uint32_t qflip, uint32_t qmask) {
   using Sh = Shape<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
 
   const uint32_t work = xcd_remap(blockIdx.x, n_wg);
-  const uint32_t per_bh = (uint32_t)F * (uint32_t)nqb;
+  const uint32_t per_bh = (uint32_t)n_items * (uint32_t)nqb;
   const uint32_t bh = work / per_bh;
   const uint32_t rem = work - bh * per_bh;
-  const int frame = order[rem / nqb];
+  const int32_t* item = items + 4 * (rem / nqb);
+  const int frame = item[0];
+  const int kbeg = item[1];
+  const int n_kept = item[2];
+  const int slot = item[3];  // >= 0: a piece of a split frame, written as a partial
   const int qb = (int)(rem % nqb);
 
   const size_t head_elems = (size_t)F * T * D;
@@ -413,8 +417,6 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   float l_run[2] = {0.f, 0.f};
   const float lazy = exp2f(kLazyLog2);
 
-  const int kbeg = row_ptr[frame];
-  const int n_kept = row_ptr[frame + 1] - kbeg;
   const int tpf = (T + kBlockK - 1) / kBlockK;
   const int n_tiles = n_kept * tpf;
 
@@ -502,37 +504,109 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     }
   }
 
-  // Epilogue: normalise, round to bf16 (RNE), store 4 consecutive d per access.
+  // Epilogue: normalise; a whole frame rounds to bf16 (RNE) into out, a piece of
+  // a split frame stores O/l in fp32 and its base-2 log-sum-exp
+  // log2(sum_t 2^(c s_t)) = c m_ref + log2(l) for the merge. 4 consecutive d per
+  // access.
 #pragma unroll
   for (int qs = 0; qs < 2; ++qs) {
     const float l_tot = pair_sum(l_run[qs]);
     const int qrow = qrow0 + 32 * qs;
     if (qrow < T) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      uint16_t* op = Oh + ((size_t)frame * T + qrow) * D;
+      if (slot < 0) {
+        uint16_t* op = Oh + ((size_t)frame * T + qrow) * D;
 #pragma unroll
-      for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+        for (int mb = 0; mb < Sh::kDBlocks; ++mb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
-                     o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
-          const bf16x4 y = __builtin_convertvector(x, bf16x4);
-          *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
-        }
+          for (int i = 0; i < 4; ++i) {
+            f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
+                       o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
+            const bf16x4 y = __builtin_convertvector(x, bf16x4);
+            *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
+          }
+      } else {
+        const size_t prow = ((size_t)slot * (n_wg / ((uint32_t)n_items * (uint32_t)nqb)) + bh) * T + qrow;
+        float* op = ws_o + prow * D;
+#pragma unroll
+        for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
+                             o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
+            *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * i + 4 * hf) = x;
+          }
+        if (hf == 0) ws_lse[prow] = m_ref[qs] * c + __builtin_amdgcn_logf(l_tot);
+      }
     }
   }
+}
+
+// Combines the pieces of split query frames. One thread per (split frame, b*h,
+// query row, 8 consecutive d): with M the largest piece log-sum-exp,
+// out = sum_p 2^(lse_p - M) (O/l)_p / sum_p 2^(lse_p - M), rounded to bf16 (RNE).
+template <int D>
+__global__ __launch_bounds__(256) void merge_partials_kernel(
+    const float* __restrict__ ws_o, const float* __restrict__ ws_lse,
+    const int32_t* __restrict__ heavy, int n_heavy, int BH, int T, uint16_t* __restrict__ O, int F) {
+  constexpr int kGroups = D / 8;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t per_frame = (size_t)BH * T * kGroups;
+  if (idx >= per_frame * (size_t)n_heavy) return;
+  const int hv = (int)(idx / per_frame);
+  const size_t r = idx - (size_t)hv * per_frame;
+  const int grp = (int)(r % kGroups);
+  const size_t row = r / kGroups;  // bh * T + t
+  const int frame = heavy[3 * hv], slot0 = heavy[3 * hv + 1], np = heavy[3 * hv + 2];
+  const size_t slot_stride = (size_t)BH * T;
+  float mx = -INFINITY;
+  for (int p = 0; p < np; ++p) mx = fmaxf(mx, ws_lse[(size_t)(slot0 + p) * slot_stride + row]);
+  f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  for (int p = 0; p < np; ++p) {
+    const size_t pr = (size_t)(slot0 + p) * slot_stride + row;
+    const float w = fast_exp2(ws_lse[pr] - mx);
+    const f32x4* src = reinterpret_cast<const f32x4*>(ws_o + pr * D + 8 * grp);
+    a0 += w * src[0];
+    a1 += w * src[1];
+    wsum += w;
+  }
+  const float inv = 1.f / wsum;
+  const size_t bh = row / T, t = row - bh * T;
+  uint16_t* op = O + ((bh * F + frame) * (size_t)T + t) * D + 8 * grp;
+  const f32x8 x = {a0[0] * inv, a0[1] * inv, a0[2] * inv, a0[3] * inv,
+                   a1[0] * inv, a1[1] * inv, a1[2] * inv, a1[3] * inv};
+  *reinterpret_cast<bf16x8*>(op) = __builtin_convertvector(x, bf16x8);
 }
 
 template <int D>
 hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
   const int nqb = (a.T + kBlockQ - 1) / kBlockQ;
   hipLaunchKernelGGL(tile_attn_fwd_kernel<D>, dim3(a.n_wg), dim3(kThreads), 0, stream, a.q, a.k,
-                     a.v, a.out, a.row_ptr, a.cols, a.order, a.F, a.T, nqb, a.n_wg, a.c, a.qflip,
-                     a.qmask);
+                     a.v, a.out, a.items, a.cols, a.n_items, a.F, a.T, nqb, a.n_wg, a.ws_o,
+                     a.ws_lse, a.c, a.qflip, a.qmask);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_merge_d(const MergeArgs& a, hipStream_t stream) {
+  const size_t threads = (size_t)a.n_heavy * a.BH * a.T * (D / 8);
+  const size_t blocks = (threads + 255) / 256;
+  hipLaunchKernelGGL(merge_partials_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.ws_o,
+                     a.ws_lse, a.heavy, a.n_heavy, a.BH, a.T, a.out, a.F);
   return hipGetLastError();
 }
 
 }  // namespace
+
+hipError_t launch_merge_partials(const MergeArgs& a, hipStream_t stream) {
+  switch (a.d) {
+    case 64: return launch_merge_d<64>(a, stream);
+    case 96: return launch_merge_d<96>(a, stream);
+    case 128: return launch_merge_d<128>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 hipError_t launch_tile_attn_fwd(const FwdArgs& a, hipStream_t stream) {
   switch (a.d) {

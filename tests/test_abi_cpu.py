@@ -101,3 +101,60 @@ def test_status_strings():
     for s in range(9):
         assert lib.tile_attn_status_string(s)
     assert lib.tile_attn_status_string(99) == b"unknown status"
+
+
+def _plan_invariants(M, items, n_slots):
+    F = M.shape[0]
+    counts = M.astype(bool).sum(axis=1)
+    row_ptr = np.concatenate([[0], np.cumsum(counts)])
+    # every kept entry of every row covered exactly once, pieces contiguous and in order
+    by_frame = {}
+    for fr, beg, cnt, slot in items:
+        by_frame.setdefault(int(fr), []).append((int(slot), int(beg), int(cnt)))
+    assert sorted(by_frame) == list(range(F))
+    used = set()
+    for fr, pieces in by_frame.items():
+        pieces.sort()
+        if len(pieces) == 1:
+            slot, beg, cnt = pieces[0]
+            assert slot == -1 and beg == row_ptr[fr] and cnt == counts[fr]
+        else:
+            assert all(s >= 0 for s, _, _ in pieces)
+            pos = row_ptr[fr]
+            for s, beg, cnt in pieces:
+                assert beg == pos and cnt >= 1
+                pos += cnt
+                used.add(s)
+            assert pos == row_ptr[fr + 1]
+    assert used == set(range(n_slots))
+    # longest items first
+    assert all(items[i, 2] >= items[i + 1, 2] for i in range(len(items) - 1))
+
+
+def test_plan_splits_only_heavy_rows():
+    M = om.tile_mask(24, 1, "sym")  # row 0 keeps 24 frames, the others 2; mean 70/24 -> 3
+    items, n_slots = ta.tile_attn_plan(M)
+    _plan_invariants(M, items, n_slots)
+    heavy = items[items[:, 0] == 0]
+    assert n_slots == 8 and len(heavy) == 8 and all(heavy[:, 2] == 3)
+    for form, g in (("col", 1), ("col", 8), ("dense", 0), ("sym", 8)):
+        M = om.tile_mask(24, g, form)
+        items, n_slots = ta.tile_attn_plan(M)
+        _plan_invariants(M, items, n_slots)
+        assert n_slots == 0 and len(items) == 24
+
+
+def test_plan_random_masks_and_caps():
+    rng = np.random.default_rng(7)
+    for F in (1, 2, 5, 33, 100):
+        for p in (0.05, 0.3, 0.9):
+            M = (rng.random((F, F)) < p).astype(np.uint8)
+            M[rng.integers(0, F)] = 1  # one dense row
+            items, n_slots = ta.tile_attn_plan(M)
+            _plan_invariants(M, items, n_slots)
+            assert all(len(items[items[:, 0] == f]) <= 32 for f in range(F))
+    M = np.ones((4, 4), np.uint8)
+    buf = np.zeros(4, np.int32)
+    n, s = ctypes.c_int(0), ctypes.c_int(0)
+    assert lib.tile_attn_plan(M.ctypes.data, 4, buf.ctypes.data, 1, ctypes.byref(n), ctypes.byref(s)) == 2
+    assert n.value == 4

@@ -240,3 +240,59 @@ def test_last_query_block_with_idle_waves():
         s = np.concatenate([f * T + rows for f in range(F)])
         ref = oa.attention_rows(qb, kb, vb, mask, T, d ** -0.5, np.zeros_like(s), np.full_like(s, h), s)
         assert_parity(got[0, h, s], ref, f"last-block-h{h}")
+
+
+# ---- split heavy query frames (partial results merged by log-sum-exp) -----------------
+
+@pytest.mark.parametrize("d", [64, 96, 128])
+def test_split_heavy_rows(d):
+    """The symmetric mask's global query frame keeps every frame: its work is split
+    into pieces whose partials are merged; every row is compared with the oracle."""
+    B, H, F, T = 2, 3, 10, 150
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=30 + d)
+    mask = om.tile_mask(F, 1, "sym")
+    assert ta.tile_attn_plan(mask)[1] > 0
+    full_check(qb, kb, vb, mask, T, d ** -0.5, f"split-d{d}")
+
+
+def test_split_random_heavy_masks():
+    rng = np.random.default_rng(31)
+    B, H, F, T, d = 1, 2, 12, 100, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=31, dist="frame_shift")
+    for trial in range(3):
+        mask = (rng.random((F, F)) < 0.2).astype(np.uint8)
+        mask[3 * trial, :] = 1
+        mask[3 * trial + 1, :] = 0  # an empty row next to a split one: zeros
+        assert ta.tile_attn_plan(mask)[1] > 0
+        full_check(qb, kb, vb, mask, T, d ** -0.5, f"split-random-{trial}")
+
+
+def test_split_on_two_streams():
+    """Each stream has its own workspace for partial results: two split calls queued
+    on two streams at once both match the oracle."""
+    B, H, F, T, d = 1, 4, 8, 300, 96
+    mask = om.tile_mask(F, 1, "sym")
+    data = [workloads.make_qkv(B, H, F, T, d, seed=40 + i) for i in range(2)]
+    dev = [tuple(to_dev(x) for x in qkv) for qkv in data]
+    outs = [torch.empty_like(dq[0]) for dq in dev]
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for rep in range(3):
+        for (q, k, v), out, s in zip(dev, outs, streams):
+            with torch.cuda.stream(s):
+                ta.tile_attn_fwd(q, k, v, out, B, H, F, T, d, mask, d ** -0.5, s)
+    torch.cuda.synchronize()
+    for (qb, kb, vb), out in zip(data, outs):
+        assert_parity(from_dev(out), oa.attention(qb, kb, vb, mask, T, d ** -0.5), "split-streams")
+
+
+def test_split_workspace_grows():
+    """A larger split call after a smaller one grows the workspace; the smaller call
+    afterwards still matches."""
+    d = 64
+    cases = [(1, 2, 6, 100), (2, 4, 9, 260), (1, 2, 6, 100)]
+    for B, H, F, T in cases:
+        qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=B * 100 + F)
+        mask = om.tile_mask(F, 1, "sym")
+        full_check(qb, kb, vb, mask, T, d ** -0.5, f"split-grow-{B}x{H}x{F}x{T}")
