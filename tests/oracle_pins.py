@@ -157,6 +157,23 @@ def pin_key_frame_permutation(attn):
     assert np.max(np.abs(a - b)) < TOL
 
 
+def pin_per_head_masks_match_sdpa(attn):
+    """An H x F x F stack applies mask h to head h (torch SDPA with that head's token
+    mask, head by head); a shared mask equals the stack of H copies."""
+    rng = np.random.default_rng(9)
+    B, H, F, T, d = 2, 3, 4, 3, 8
+    q, k, v = (_rand(rng, B, H, F * T, d) for _ in range(3))
+    masks = (rng.random((H, F, F)) < 0.5).astype(np.uint8)
+    masks[1, 2, :] = 0
+    got = attn(q, k, v, masks, T, 0.6)
+    for h in range(H):
+        ref = _sdpa_masked(q[:, h:h + 1], k[:, h:h + 1], v[:, h:h + 1], masks[h], T, 0.6)
+        assert np.max(np.abs(got[:, h:h + 1] - ref)) < TOL, f"head {h}"
+    shared = attn(q, k, v, masks[0], T, 0.6)
+    stacked = attn(q, k, v, np.stack([masks[0]] * H), T, 0.6)
+    assert np.max(np.abs(shared - stacked)) < TOL
+
+
 ALL_PINS = [
     pin_dense_matches_sdpa,
     pin_all_small_masks_match_sdpa,
@@ -166,4 +183,52 @@ ALL_PINS = [
     pin_uniform_weights,
     pin_identical_frames,
     pin_key_frame_permutation,
+    pin_per_head_masks_match_sdpa,
 ]
+
+
+# ---- pins of the log-sum-exp output: lse(q, k, mask, T, scale) -> [B, H, S] --------
+
+def pin_lse_dense_matches_logsumexp(lse):
+    rng = np.random.default_rng(10)
+    B, H, F, T, d = 1, 2, 3, 4, 8
+    q, k = (_rand(rng, B, H, F * T, d) for _ in range(2))
+    scale = 0.45
+    ref = torch.logsumexp(scale * torch.from_numpy(q) @ torch.from_numpy(k).transpose(-1, -2), dim=-1).numpy()
+    got = lse(q, k, np.ones((F, F), np.uint8), T, scale)
+    assert np.max(np.abs(got - ref)) < TOL
+
+
+def pin_lse_bruteforce(lse):
+    """Pure-Python log(sum(exp)) over the kept keys, -inf for rows keeping nothing,
+    with a different mask per head."""
+    rng = np.random.default_rng(11)
+    H, F, T, d = 2, 3, 2, 3
+    masks = np.array([[[1, 0, 1], [0, 0, 0], [1, 1, 0]], [[0, 1, 0], [1, 1, 1], [0, 0, 1]]], np.uint8)
+    q, k = (_rand(rng, 1, H, F * T, d) for _ in range(2))
+    got = lse(q, k, masks, T, 1.3)
+    for h in range(H):
+        for s in range(F * T):
+            kept = [t for t in range(F * T) if masks[h][s // T][t // T]]
+            if not kept:
+                assert got[0, h, s] == -np.inf
+                continue
+            z = sum(math.exp(1.3 * sum(q[0, h, s, c] * k[0, h, t, c] for c in range(d))) for t in kept)
+            assert abs(got[0, h, s] - math.log(z)) < TOL, (h, s)
+
+
+def pin_lse_uniform(lse):
+    """Q = 0: every logit is 0, so lse = log(number of kept keys) = log(T * kept frames)."""
+    rng = np.random.default_rng(12)
+    F, T, d = 5, 7, 4
+    mask = (rng.random((F, F)) < 0.5).astype(np.uint8)
+    mask[0, :] = 1
+    k = _rand(rng, 1, 1, F * T, d)
+    got = lse(np.zeros_like(k), k, mask, T, 0.9)
+    for i in range(F):
+        n = int(mask[i].sum())
+        expect = math.log(T * n) if n else -np.inf
+        assert np.all(got[0, 0, i * T:(i + 1) * T] == expect) or np.max(np.abs(got[0, 0, i * T:(i + 1) * T] - expect)) < TOL
+
+
+LSE_PINS = [pin_lse_dense_matches_logsumexp, pin_lse_bruteforce, pin_lse_uniform]

@@ -46,6 +46,25 @@ def test_uint16_input_equals_float_input():
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("pin", oracle_pins.LSE_PINS, ids=lambda f: f.__name__)
+def test_oracle_lse_pin(pin):
+    pin(oa.attention_lse)
+
+
+def test_lse_matches_attention_normaliser():
+    """The same weights normalise the output: with V = e_j (one-hot columns) the output is
+    the softmax itself, whose log at the max logit equals max - lse."""
+    rng = np.random.default_rng(13)
+    F, T, d = 3, 4, 5
+    mask = np.array([[1, 1, 0], [0, 1, 1], [1, 0, 1]], np.uint8)
+    q, k = rng.standard_normal((2, 1, 1, F * T, d))
+    lse = oa.attention_lse(q, k, mask, T, 0.7)
+    for s in range(F * T):
+        kept = [t for t in range(F * T) if mask[s // T][t // T]]
+        logits = [0.7 * float(q[0, 0, s] @ k[0, 0, t]) for t in kept]
+        assert abs(sum(np.exp(np.array(logits) - lse[0, 0, s])) - 1.0) < 1e-12
+
+
 # Planted mistakes: each mutant of the oracle source must fail at least one pin.
 MUTANTS = [
     ("transposed mask", "mask[i, j]", "mask[j, i]"),
@@ -57,6 +76,10 @@ MUTANTS = [
      "out[b, h, rows] = _softmax_rows_times_v(logits, kh[cols])"),
     ("query rows of the wrong frame", "rows = frame_tokens(i, T)", "rows = frame_tokens((i + 1) % F, T)"),
     ("query and key swapped", "logits = scale * (qh[rows] @ kh[cols].T)", "logits = scale * (kh[rows] @ qh[cols].T)"),
+    ("mask of head 0 for every head", "return mask if mask.ndim == 2 else mask[h]",
+     "return mask if mask.ndim == 2 else mask[0]"),
+    ("log2 in the log-sum-exp", "m + np.log(np.exp(logits - m)", "m + np.log2(np.exp(logits - m)"),
+    ("lse without the max shift", "lse[b, h, rows] = (m + np.log(", "lse[b, h, rows] = (np.log("),
 ]
 
 
@@ -77,6 +100,11 @@ def test_pins_catch_planted_mistake(name, old, new):
     for pin in oracle_pins.ALL_PINS:
         try:
             pin(mutant.attention)
+        except Exception:
+            failures += 1
+    for pin in oracle_pins.LSE_PINS:
+        try:
+            pin(mutant.attention_lse)
         except Exception:
             failures += 1
     assert failures > 0, f"no pin caught the planted mistake: {name}"
