@@ -79,6 +79,29 @@ int tile_attn_fwd(const void* q, const void* k, const void* v, void* out,
                   const uint8_t* tile_mask, float scale, void* stream);
 
 /*
+ * Tile-sparse attention forward with one mask per head and an optional row
+ * log-sum-exp. The layer-wise search of Sec. 3.3 (Alg. 1) gives each layer, and
+ * the heads within it, their own k:(F-k) pattern; the log-sum-exp is what a
+ * merge of partial results or a backward pass needs.
+ *
+ * tile_masks: HOST pointer to n_masks * F * F bytes, mask after mask, each
+ *   row-major [query_frame][key_frame], nonzero = kept; n_masks == 1 shares one
+ *   mask across all heads (tile_attn_fwd), n_masks == H gives mask h to head h.
+ *   Read during the call only.
+ * lse: DEVICE pointer to fp32 [B, H, S], 4-byte aligned, or NULL. Receives for each
+ *   query token the natural-log log-sum-exp of scale * <q, k_t> over its kept keys
+ *   t (computed from the bf16-rounded weights that also weight V), and -inf for a
+ *   query frame that keeps nothing. Must not overlap q, k, v or out.
+ * Errors: those of tile_attn_fwd, plus TA_ERR_BAD_MASK when n_masks is neither 1
+ *   nor H, TA_ERR_ALIGN for a misaligned lse and TA_ERR_OVERLAP when lse overlaps
+ *   a tensor.
+ */
+int tile_attn_fwd_heads(const void* q, const void* k, const void* v, void* out,
+                        int B, int H, int F, int T, int d,
+                        const uint8_t* tile_masks, int n_masks, float scale,
+                        float* lse, void* stream);
+
+/*
  * Dense control: 3D full attention (every tile kept, the "full" rows of
  * tab:kernel_time). Runs the same kernel as tile_attn_fwd with an all-ones
  * mask, so its output is bit-identical to tile_attn_fwd with that mask.

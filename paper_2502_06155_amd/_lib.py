@@ -12,6 +12,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtileattn
 
 EXPORTS = (
     "tile_attn_fwd",
+    "tile_attn_fwd_heads",
     "dense_attn_fwd",
     "tile_attn_make_mask",
     "tile_attn_compact",
@@ -47,6 +48,8 @@ def _load() -> ctypes.CDLL:
     vp, ci, cf = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
     lib.tile_attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, vp, cf, vp]
     lib.tile_attn_fwd.restype = ci
+    lib.tile_attn_fwd_heads.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, vp, ci, cf, vp, vp]
+    lib.tile_attn_fwd_heads.restype = ci
     lib.dense_attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp]
     lib.dense_attn_fwd.restype = ci
     lib.tile_attn_make_mask.argtypes = [ci, ci, ci, vp]

@@ -61,6 +61,19 @@ def tile_attn_fwd(q, k, v, out, B: int, H: int, F: int, T: int, d: int, tile_mas
                              m.ctypes.data, float(scale), _stream(stream)), "tile_attn_fwd")
 
 
+def tile_attn_fwd_heads(q, k, v, out, B: int, H: int, F: int, T: int, d: int, tile_masks,
+                        scale: float, lse=None, stream=None) -> None:
+    """tile_attn_fwd_heads of the C ABI: tile_masks is F x F (shared) or H x F x F (one
+    per head); lse is an optional fp32 [B, H, F*T] device tensor or address."""
+    m = np.ascontiguousarray(np.asarray(tile_masks), dtype=np.uint8)
+    if m.size % (F * F):
+        raise ValueError("tile_masks must hold n_masks * F * F entries")
+    n_masks = m.size // (F * F)
+    _check(lib.tile_attn_fwd_heads(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, F, T, d,
+                                   m.ctypes.data, n_masks, float(scale), _ptr(lse),
+                                   _stream(stream)), "tile_attn_fwd_heads")
+
+
 def dense_attn_fwd(q, k, v, out, B: int, H: int, F: int, T: int, d: int, scale: float,
                    stream=None) -> None:
     """dense_attn_fwd of the C ABI: every tile kept."""

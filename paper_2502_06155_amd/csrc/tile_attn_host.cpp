@@ -98,8 +98,10 @@ WorkPlan plan_work(const uint8_t* mask, int F, bool allow_split) {
   return pl;
 }
 
-// A work plan resident on one device: [items][cols][heavy] in int32 words, read
-// by the kernels with scalar loads.
+// The work plans of all heads resident on one device: [items][cols][heavy] in int32
+// words, read by the kernels with scalar loads. Items are {head, frame, first kept
+// entry, count, slot} with cols and slots offset per head; heavy entries are
+// {head, frame, first slot, slots}.
 struct DeviceWorkList {
   void* buffer = nullptr;
   const int32_t* items = nullptr;
@@ -149,26 +151,48 @@ int check_args(const void* q, const void* k, const void* v, void* out, int B, in
   return TA_OK;
 }
 
-// Returns the device-resident work list for `mask` (split or not), uploading it on
-// first use on the current device.
-int work_list_for(const uint8_t* mask, int F, bool allow_split, int dev,
+// Returns the device-resident work list for H heads with n_masks masks (1: shared,
+// H: one per head), split or not, uploading it on first use on device dev.
+int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_split, int dev,
                   const DeviceWorkList** out) {
-  std::string key(reinterpret_cast<const char*>(mask), (size_t)F * F);
-  key.push_back(allow_split ? 's' : 'u');
+  std::string key(reinterpret_cast<const char*>(masks), (size_t)n_masks * F * F);
+  key += allow_split ? "|s|" : "|u|";
+  key += std::to_string(H) + "|" + std::to_string(n_masks);
   std::lock_guard<std::mutex> lock(g_cache_mutex);
   auto it = g_cache.find({dev, key});
   if (it != g_cache.end()) {
     *out = &it->second;
     return TA_OK;
   }
-  const WorkPlan pl = plan_work(mask, F, allow_split);
+  std::vector<int32_t> items, cols, heavy;
+  int n_slots = 0;
+  WorkPlan shared;
+  if (n_masks == 1) {
+    shared = plan_work(masks, F, allow_split);
+    cols = shared.cols;
+  }
+  for (int h = 0; h < H; ++h) {
+    WorkPlan own;
+    if (n_masks != 1) own = plan_work(masks + (size_t)h * F * F, F, allow_split);
+    const WorkPlan& pl = n_masks == 1 ? shared : own;
+    const int col_off = n_masks == 1 ? 0 : (int)cols.size();
+    if (n_masks != 1) cols.insert(cols.end(), pl.cols.begin(), pl.cols.end());
+    for (size_t i = 0; i < pl.items.size(); i += 4) {
+      const int slot = pl.items[i + 3];
+      items.insert(items.end(), {h, pl.items[i], pl.items[i + 1] + col_off, pl.items[i + 2],
+                                 slot < 0 ? -1 : slot + n_slots});
+    }
+    for (size_t i = 0; i < pl.heavy.size(); i += 3)
+      heavy.insert(heavy.end(), {h, pl.heavy[i], pl.heavy[i + 1] + n_slots, pl.heavy[i + 2]});
+    n_slots += pl.n_slots;
+  }
   std::vector<int32_t> words;
-  words.insert(words.end(), pl.items.begin(), pl.items.end());
+  words.insert(words.end(), items.begin(), items.end());
   const size_t off_cols = words.size();
-  words.insert(words.end(), pl.cols.begin(), pl.cols.end());
+  words.insert(words.end(), cols.begin(), cols.end());
   const size_t off_heavy = words.size();
-  words.insert(words.end(), pl.heavy.begin(), pl.heavy.end());
-  if (pl.heavy.empty()) words.push_back(0);
+  words.insert(words.end(), heavy.begin(), heavy.end());
+  if (heavy.empty()) words.push_back(0);
   const size_t total = words.size() * sizeof(int32_t);
   void* buf = nullptr;
   hipError_t e = hipMalloc(&buf, total);
@@ -183,9 +207,9 @@ int work_list_for(const uint8_t* mask, int F, bool allow_split, int dev,
   entry.items = static_cast<const int32_t*>(buf);
   entry.cols = static_cast<const int32_t*>(buf) + off_cols;
   entry.heavy = static_cast<const int32_t*>(buf) + off_heavy;
-  entry.n_items = (int)(pl.items.size() / 4);
-  entry.n_heavy = (int)(pl.heavy.size() / 3);
-  entry.n_slots = pl.n_slots;
+  entry.n_items = (int)(items.size() / 5);
+  entry.n_heavy = (int)(heavy.size() / 4);
+  entry.n_slots = n_slots;
   auto res = g_cache.emplace(std::make_pair(dev, std::move(key)), entry);
   *out = &res.first->second;
   return TA_OK;
@@ -211,23 +235,23 @@ int workspace_for(int dev, void* stream, size_t bytes, void** out) {
 }
 
 int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F, int T,
-            int d, const uint8_t* mask, float scale, void* stream) {
+            int d, const uint8_t* masks, int n_masks, float scale, float* lse, void* stream) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
   const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
   const DeviceWorkList* wl = nullptr;
-  int st = work_list_for(mask, F, true, dev, &wl);
+  int st = work_list_for(masks, n_masks, H, F, true, dev, &wl);
   if (st != TA_OK) return st;
-  const size_t ws_bytes = (size_t)wl->n_slots * B * H * T * (d + 1) * sizeof(float);
   const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
-  if (ws_bytes > kMaxWorkspaceBytes || (int64_t)B * H * wl->n_items * nqb > max_wg) {
-    st = work_list_for(mask, F, false, dev, &wl);  // the same frames, not split
+  if ((size_t)wl->n_slots * B * T * (d + 1) * sizeof(float) > kMaxWorkspaceBytes ||
+      (int64_t)B * wl->n_items * nqb > max_wg) {
+    st = work_list_for(masks, n_masks, H, F, false, dev, &wl);  // the same frames, not split
     if (st != TA_OK) return st;
   }
   void* ws = nullptr;
   if (wl->n_slots > 0) {
-    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * H * T * (d + 1) * sizeof(float), &ws);
+    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * T * (d + 1) * sizeof(float), &ws);
     if (st != TA_OK) return st;
   }
   ta::FwdArgs a;
@@ -244,7 +268,8 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   a.cols = wl->cols;
   a.n_items = wl->n_items;
   a.ws_o = static_cast<float*>(ws);
-  a.ws_lse = ws ? static_cast<float*>(ws) + (size_t)wl->n_slots * B * H * T * d : nullptr;
+  a.ws_lse = ws ? static_cast<float*>(ws) + (size_t)wl->n_slots * B * T * d : nullptr;
+  a.lse = lse;
   // Logits are formed from |scale| (a negative scale flips the sign of q, which
   // is exact in bf16). scale == 0 zeroes q instead, so every logit is exactly 0
   // and the weights exactly uniform; c only has to stay positive.
@@ -257,7 +282,7 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
     a.qflip = std::signbit(scale) ? 0x80008000u : 0u;
     a.qmask = 0xFFFFFFFFu;
   }
-  a.n_wg = (uint32_t)((int64_t)B * H * wl->n_items * nqb);
+  a.n_wg = (uint32_t)((int64_t)B * wl->n_items * nqb);
   e = ta::launch_tile_attn_fwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
   if (wl->n_heavy > 0) {
@@ -266,11 +291,13 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
     m.ws_lse = a.ws_lse;
     m.heavy = wl->heavy;
     m.n_heavy = wl->n_heavy;
-    m.BH = B * H;
+    m.B = B;
+    m.H = H;
     m.F = F;
     m.T = T;
     m.d = d;
     m.out = a.out;
+    m.lse = lse;
     e = ta::launch_merge_partials(m, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
   }
@@ -331,7 +358,24 @@ int tile_attn_fwd(const void* q, const void* k, const void* v, void* out, int B,
   int st = check_args(q, k, v, out, B, H, F, T, d, scale);
   if (st != TA_OK) return st;
   if (!tile_mask) return fail(TA_ERR_NULL_PTR, "tile_mask must be non-NULL");
-  return run_fwd(q, k, v, out, B, H, F, T, d, tile_mask, scale, stream);
+  return run_fwd(q, k, v, out, B, H, F, T, d, tile_mask, 1, scale, nullptr, stream);
+}
+
+int tile_attn_fwd_heads(const void* q, const void* k, const void* v, void* out, int B, int H,
+                        int F, int T, int d, const uint8_t* tile_masks, int n_masks, float scale,
+                        float* lse, void* stream) {
+  int st = check_args(q, k, v, out, B, H, F, T, d, scale);
+  if (st != TA_OK) return st;
+  if (!tile_masks) return fail(TA_ERR_NULL_PTR, "tile_masks must be non-NULL");
+  if (n_masks != 1 && n_masks != H) return fail(TA_ERR_BAD_MASK, "n_masks must be 1 or H");
+  if (lse) {
+    if (reinterpret_cast<uintptr_t>(lse) % 4) return fail(TA_ERR_ALIGN, "lse must be 4-byte aligned");
+    const size_t bytes = (size_t)B * H * F * T * d * 2;
+    const size_t lbytes = (size_t)B * H * F * T * sizeof(float);
+    for (const void* p : {q, k, v, (const void*)out})
+      if (ranges_overlap(lse, lbytes, p, bytes)) return fail(TA_ERR_OVERLAP, "lse overlaps a tensor");
+  }
+  return run_fwd(q, k, v, out, B, H, F, T, d, tile_masks, n_masks, scale, lse, stream);
 }
 
 int dense_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
@@ -339,7 +383,7 @@ int dense_attn_fwd(const void* q, const void* k, const void* v, void* out, int B
   int st = check_args(q, k, v, out, B, H, F, T, d, scale);
   if (st != TA_OK) return st;
   std::vector<uint8_t> ones((size_t)F * F, 1);
-  return run_fwd(q, k, v, out, B, H, F, T, d, ones.data(), scale, stream);
+  return run_fwd(q, k, v, out, B, H, F, T, d, ones.data(), 1, scale, nullptr, stream);
 }
 
 const char* tile_attn_status_string(int status) {

@@ -360,22 +360,23 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int F,
-    int T, int nqb, uint32_t n_wg, float* __restrict__ ws_o, float* __restrict__ ws_lse,
-    float c, uint32_t qflip, uint32_t qmask) {
+    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int H,
+    int F, int T, int nqb, uint32_t n_wg, float* __restrict__ ws_o, float* __restrict__ ws_lse,
+    float* __restrict__ lse, float c, uint32_t qflip, uint32_t qmask) {
   using Sh = Shape<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
 
   const uint32_t work = xcd_remap(blockIdx.x, n_wg);
-  const uint32_t per_bh = (uint32_t)n_items * (uint32_t)nqb;
-  const uint32_t bh = work / per_bh;
-  const uint32_t rem = work - bh * per_bh;
-  const int32_t* item = items + 4 * (rem / nqb);
-  const int frame = item[0];
-  const int kbeg = item[1];
-  const int n_kept = item[2];
-  const int slot = item[3];  // >= 0: a piece of a split frame, written as a partial
+  const uint32_t per_b = (uint32_t)n_items * (uint32_t)nqb;
+  const uint32_t b = work / per_b;
+  const uint32_t rem = work - b * per_b;
+  const int32_t* item = items + 5 * (rem / nqb);
+  const uint32_t bh = b * (uint32_t)H + (uint32_t)item[0];
+  const int frame = item[1];
+  const int kbeg = item[2];
+  const int n_kept = item[3];
+  const int slot = item[4];  // >= 0: a piece of a split frame, written as a partial
   const int qb = (int)(rem % nqb);
 
   const size_t head_elems = (size_t)F * T * D;
@@ -525,8 +526,13 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
             const bf16x4 y = __builtin_convertvector(x, bf16x4);
             *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
           }
+        if (lse && hf == 0)
+          lse[((size_t)bh * F + frame) * T + qrow] =
+              l_tot > 0.f ? (m_ref[qs] * c + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f
+                          : -INFINITY;
       } else {
-        const size_t prow = ((size_t)slot * (n_wg / ((uint32_t)n_items * (uint32_t)nqb)) + bh) * T + qrow;
+        const uint32_t nb = n_wg / per_b;  // batch size
+        const size_t prow = ((size_t)slot * nb + b) * T + qrow;
         float* op = ws_o + prow * D;
 #pragma unroll
         for (int mb = 0; mb < Sh::kDBlocks; ++mb)
@@ -542,23 +548,26 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   }
 }
 
-// Combines the pieces of split query frames. One thread per (split frame, b*h,
-// query row, 8 consecutive d): with M the largest piece log-sum-exp,
-// out = sum_p 2^(lse_p - M) (O/l)_p / sum_p 2^(lse_p - M), rounded to bf16 (RNE).
+// Combines the pieces of split query frames. One thread per (split frame, batch
+// entry, query row, 8 consecutive d): with M the largest piece log-sum-exp,
+// out = sum_p 2^(lse_p - M) (O/l)_p / sum_p 2^(lse_p - M), rounded to bf16 (RNE);
+// the row's log-sum-exp is M + log2(sum_p 2^(lse_p - M)), stored in natural log.
 template <int D>
 __global__ __launch_bounds__(256) void merge_partials_kernel(
     const float* __restrict__ ws_o, const float* __restrict__ ws_lse,
-    const int32_t* __restrict__ heavy, int n_heavy, int BH, int T, uint16_t* __restrict__ O, int F) {
+    const int32_t* __restrict__ heavy, int n_heavy, int B, int H, int F, int T,
+    uint16_t* __restrict__ O, float* __restrict__ lse) {
   constexpr int kGroups = D / 8;
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t per_frame = (size_t)BH * T * kGroups;
+  const size_t per_frame = (size_t)B * T * kGroups;
   if (idx >= per_frame * (size_t)n_heavy) return;
   const int hv = (int)(idx / per_frame);
   const size_t r = idx - (size_t)hv * per_frame;
   const int grp = (int)(r % kGroups);
-  const size_t row = r / kGroups;  // bh * T + t
-  const int frame = heavy[3 * hv], slot0 = heavy[3 * hv + 1], np = heavy[3 * hv + 2];
-  const size_t slot_stride = (size_t)BH * T;
+  const size_t row = r / kGroups;  // b * T + t
+  const int head = heavy[4 * hv], frame = heavy[4 * hv + 1];
+  const int slot0 = heavy[4 * hv + 2], np = heavy[4 * hv + 3];
+  const size_t slot_stride = (size_t)B * T;
   float mx = -INFINITY;
   for (int p = 0; p < np; ++p) mx = fmaxf(mx, ws_lse[(size_t)(slot0 + p) * slot_stride + row]);
   f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
@@ -572,28 +581,29 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(
     wsum += w;
   }
   const float inv = 1.f / wsum;
-  const size_t bh = row / T, t = row - bh * T;
-  uint16_t* op = O + ((bh * F + frame) * (size_t)T + t) * D + 8 * grp;
+  const size_t b = row / T, t = row - b * T;
+  const size_t orow = ((b * H + head) * F + frame) * (size_t)T + t;
   const f32x8 x = {a0[0] * inv, a0[1] * inv, a0[2] * inv, a0[3] * inv,
                    a1[0] * inv, a1[1] * inv, a1[2] * inv, a1[3] * inv};
-  *reinterpret_cast<bf16x8*>(op) = __builtin_convertvector(x, bf16x8);
+  *reinterpret_cast<bf16x8*>(O + orow * D + 8 * grp) = __builtin_convertvector(x, bf16x8);
+  if (lse && grp == 0) lse[orow] = (mx + __builtin_amdgcn_logf(wsum)) * 0.69314718055994531f;
 }
 
 template <int D>
 hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
   const int nqb = (a.T + kBlockQ - 1) / kBlockQ;
   hipLaunchKernelGGL(tile_attn_fwd_kernel<D>, dim3(a.n_wg), dim3(kThreads), 0, stream, a.q, a.k,
-                     a.v, a.out, a.items, a.cols, a.n_items, a.F, a.T, nqb, a.n_wg, a.ws_o,
-                     a.ws_lse, a.c, a.qflip, a.qmask);
+                     a.v, a.out, a.items, a.cols, a.n_items, a.H, a.F, a.T, nqb, a.n_wg, a.ws_o,
+                     a.ws_lse, a.lse, a.c, a.qflip, a.qmask);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_merge_d(const MergeArgs& a, hipStream_t stream) {
-  const size_t threads = (size_t)a.n_heavy * a.BH * a.T * (D / 8);
+  const size_t threads = (size_t)a.n_heavy * a.B * a.T * (D / 8);
   const size_t blocks = (threads + 255) / 256;
   hipLaunchKernelGGL(merge_partials_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.ws_o,
-                     a.ws_lse, a.heavy, a.n_heavy, a.BH, a.T, a.out, a.F);
+                     a.ws_lse, a.heavy, a.n_heavy, a.B, a.H, a.F, a.T, a.out, a.lse);
   return hipGetLastError();
 }
 

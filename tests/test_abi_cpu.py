@@ -158,3 +158,22 @@ def test_plan_random_masks_and_caps():
     n, s = ctypes.c_int(0), ctypes.c_int(0)
     assert lib.tile_attn_plan(M.ctypes.data, 4, buf.ctypes.data, 1, ctypes.byref(n), ctypes.byref(s)) == 2
     assert n.value == 4
+
+
+def _heads(q=1 << 12, k=2 << 12, v=3 << 12, out=4 << 12, B=1, H=2, F=2, T=8, d=64, masks=None,
+           n=None, lse=None,
+           scale=0.125):
+    m = np.ones((H, F, F), np.uint8) if masks is None else masks
+    nm = m.size // (F * F) if n is None else n
+    return lib.tile_attn_fwd_heads(q, k, v, out, B, H, F, T, d, m.ctypes.data, nm, scale, lse, None)
+
+
+def test_heads_argument_errors_before_any_gpu_call():
+    assert _heads(n=3) == 4 and _heads(n=0) == 4  # n_masks neither 1 nor H
+    assert _heads(q=1 << 13, k=2 << 13, v=3 << 13, out=4 << 13, masks=np.ones((1, 2, 2), np.uint8), n=2, H=3) == 4
+    assert lib.tile_attn_fwd_heads(1 << 12, 2 << 12, 3 << 12, 4 << 12, 1, 2, 2, 8, 64, None, 2, 0.1,
+                                   None, None) == 1
+    assert _heads(lse=1 << 20 | 2) == 5  # misaligned lse
+    assert _heads(lse=(2 << 12) + 64) == 7  # lse overlaps k
+    assert "overlap" in lib.tile_attn_last_error().decode()
+    assert _heads(d=80) == 3 and _heads(B=0) == 2

@@ -296,3 +296,83 @@ def test_split_workspace_grows():
         qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=B * 100 + F)
         mask = om.tile_mask(F, 1, "sym")
         full_check(qb, kb, vb, mask, T, d ** -0.5, f"split-grow-{B}x{H}x{F}x{T}")
+
+
+# ---- one mask per head and the row log-sum-exp ----------------------------------------
+
+LSE_MAX_ABS = 5e-3  # natural-log units; the GPU sums the bf16-rounded weights
+
+
+def run_gpu_heads(qb, kb, vb, masks, T, scale):
+    B, H, S, d = qb.shape
+    F = S // T
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    out = torch.empty_like(q)
+    lse = torch.full((B, H, S), 12345.0, dtype=torch.float32, device="cuda")
+    ta.tile_attn_fwd_heads(q, k, v, out, B, H, F, T, d, masks, scale, lse,
+                           torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    return from_dev(out), lse.cpu().numpy().astype(np.float64)
+
+
+def assert_lse(got, ref, what):
+    empty = np.isneginf(ref)
+    assert np.array_equal(np.isneginf(got), empty), f"{what}: -inf rows differ"
+    err = np.abs(got[~empty] - ref[~empty])
+    print(f"[lse] {what} max abs {err.max() if err.size else 0.0:.2e}", flush=True)
+    assert err.size == 0 or err.max() <= LSE_MAX_ABS, f"{what}: lse max abs {err.max()}"
+
+
+def _head_masks(F):
+    rng = np.random.default_rng(F)
+    rand = (rng.random((F, F)) < 0.4).astype(np.uint8)
+    rand[1, :] = 0
+    return np.stack([np.ones((F, F), np.uint8), om.tile_mask(F, 1, "col"),
+                     om.tile_mask(F, 1, "sym"), rand])
+
+
+@pytest.mark.parametrize("d", [64, 96, 128])
+def test_per_head_masks_and_lse(d):
+    B, H, F, T = 2, 4, 7, 130
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=50 + d, dist="frame_shift")
+    masks = _head_masks(F)
+    got, lse = run_gpu_heads(qb, kb, vb, masks, T, d ** -0.5)
+    assert_parity(got, oa.attention(qb, kb, vb, masks, T, d ** -0.5), f"heads-d{d}")
+    assert_lse(lse, oa.attention_lse(qb, kb, masks, T, d ** -0.5), f"heads-d{d}")
+
+
+def test_shared_mask_heads_matches_tile_attn_fwd_bitwise():
+    B, H, F, T, d = 1, 3, 6, 200, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=55)
+    for form in ("col", "sym"):
+        mask = om.tile_mask(F, 2, form)
+        a = run_gpu(qb, kb, vb, mask, T, d ** -0.5)
+        b, lse = run_gpu_heads(qb, kb, vb, mask, T, d ** -0.5)
+        assert np.array_equal(a, b), form
+        assert_lse(lse, oa.attention_lse(qb, kb, mask, T, d ** -0.5), f"shared-{form}")
+
+
+@pytest.mark.parametrize("scale", [-0.1, 0.0, 0.35])
+def test_lse_scales(scale):
+    B, H, F, T, d = 1, 2, 5, 70, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=56)
+    masks = np.stack([om.tile_mask(F, 1, "sym"), om.tile_mask(F, 2, "col")])
+    got, lse = run_gpu_heads(qb, kb, vb, masks, T, scale)
+    assert_parity(got, oa.attention(qb, kb, vb, masks, T, scale), f"lse-scale{scale}")
+    assert_lse(lse, oa.attention_lse(qb, kb, masks, T, scale), f"lse-scale{scale}")
+
+
+def test_per_head_masks_full_size_sampled():
+    """93-frame 720p shape with a different k:(F-k) pattern per head (col and sym, g = 1,
+    2, 4, 8): sampled rows of every head, and the log-sum-exp of two heads in full."""
+    w = workloads.WORKLOADS["93f"]
+    qb, kb, vb = _inputs(w)
+    masks = np.stack([om.tile_mask(w.F, [1, 2, 4, 8][h % 4], "col" if h % 2 else "sym")
+                      for h in range(w.H)])
+    got, lse = run_gpu_heads(qb, kb, vb, masks, w.T, w.scale())
+    b, h, s = sample_rows(w.B, w.H, w.F, w.T, per_frame=2, seed=57)
+    ref = oa.attention_rows(qb, kb, vb, masks, w.T, w.scale(), b, h, s)
+    assert_parity(got[b, h, s], ref, "heads-93f")
+    for hh in (0, 5):
+        ref_lse = oa.attention_lse(qb[:, hh:hh + 1], kb[:, hh:hh + 1], masks[hh], w.T, w.scale())
+        assert_lse(lse[:, hh:hh + 1], ref_lse, f"heads-93f-lse-h{hh}")
