@@ -1,0 +1,58 @@
+"""Gradients of tile-sparse 3D attention, written out from their definition (oracle side).
+
+Test infrastructure only; see the package docstring.
+
+The forward output of query token s (Sec. 3.3; ``oracle.attention``) is
+out_s = sum_t P_st v_t with P_st = softmax_t(scale * <q_s, k_t>) over the keys t
+of the frames that s's frame keeps. Its gradients, for an upstream gradient dO,
+follow from the chain rule through the softmax (the training of the sparse
+student in Sec. 3.4 back-propagates through this operation):
+
+    dP_st = <dO_s, v_t>
+    dS_st = P_st * (dP_st - D_s),  D_s = sum_t P_st dP_st = <dO_s, out_s>
+    dq_s  = scale * sum_t dS_st k_t
+    dk_t  = scale * sum_s dS_st q_s
+    dv_t  = sum_s P_st dO_s
+
+with sums over kept pairs only. Keys of frames nobody keeps get zero gradient,
+and so do queries of frames that keep nothing. A mask is F x F (shared by the
+heads) or H x F x F (one per head). Arithmetic is float64.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .attention import as_f64, frame_tokens, head_mask, kept_frames
+
+
+def attention_backward(q, k, v, dout, mask, T: int, scale: float):
+    """(dq, dk, dv), each float64 [B, H, S, d], for upstream gradient dout."""
+    mask = np.asarray(mask)
+    B, H, S, d = np.shape(q)
+    F = S // T
+    if F * T != S or mask.shape not in ((F, F), (H, F, F)):
+        raise ValueError("q must be [B, H, F*T, d] and mask F x F or H x F x F")
+    dq = np.zeros((B, H, S, d))
+    dk = np.zeros((B, H, S, d))
+    dv = np.zeros((B, H, S, d))
+    for b in range(B):
+        for h in range(H):
+            qh, kh, vh, gh = (as_f64(x[b, h]) for x in (q, k, v, dout))
+            mh = head_mask(mask, h)
+            for i in range(F):
+                kept = kept_frames(mh, i)
+                if not kept:
+                    continue
+                rows = frame_tokens(i, T)
+                cols = np.concatenate([frame_tokens(j, T) for j in kept])
+                logits = scale * (qh[rows] @ kh[cols].T)
+                w = np.exp(logits - logits.max(axis=-1, keepdims=True))
+                p = w / w.sum(axis=-1, keepdims=True)
+                out = p @ vh[cols]
+                dp = gh[rows] @ vh[cols].T
+                big_d = (gh[rows] * out).sum(axis=-1, keepdims=True)
+                ds = p * (dp - big_d)
+                dq[b, h, rows] += scale * (ds @ kh[cols])
+                dk[b, h, cols] += scale * (ds.T @ qh[rows])
+                dv[b, h, cols] += p.T @ gh[rows]
+    return dq, dk, dv

@@ -232,3 +232,91 @@ def pin_lse_uniform(lse):
 
 
 LSE_PINS = [pin_lse_dense_matches_logsumexp, pin_lse_bruteforce, pin_lse_uniform]
+
+
+# ---- pins of the gradients: bwd(q, k, v, dout, mask, T, scale) -> (dq, dk, dv) -------
+
+def _autograd_masked(q, k, v, dout, mask, T, scale):
+    """torch autograd (float64) through SDPA with the token mask of each head; rows that
+    keep nothing contribute nothing."""
+    B, H, S, d = q.shape
+    F = S // T
+    frame = np.arange(S) // T
+    grads = [np.zeros_like(q) for _ in range(3)]
+    for h in range(H):
+        m = np.asarray(mask if np.ndim(mask) == 2 else mask[h], dtype=bool)
+        tok = m[frame][:, frame]
+        empty = ~tok.any(axis=1)
+        tok[empty, :] = True
+        qt, kt, vt = (torch.tensor(x[:, h:h + 1], requires_grad=True) for x in (q, k, v))
+        out = torch.nn.functional.scaled_dot_product_attention(
+            qt, kt, vt, attn_mask=torch.from_numpy(tok), scale=scale)
+        g = torch.from_numpy(dout[:, h:h + 1].copy())
+        g[:, :, torch.from_numpy(empty)] = 0.0
+        out.backward(g)
+        for dst, t in zip(grads, (qt, kt, vt)):
+            dst[:, h:h + 1] = t.grad.numpy()
+    return grads
+
+
+def pin_bwd_matches_autograd(bwd):
+    rng = np.random.default_rng(20)
+    for (B, H, F, T, d, p) in [(1, 2, 3, 4, 8, 1.0), (2, 2, 4, 3, 4, 0.5), (1, 3, 5, 2, 6, 0.3)]:
+        q, k, v, g = (_rand(rng, B, H, F * T, d) for _ in range(4))
+        masks = (rng.random((H, F, F)) < p).astype(np.uint8)
+        masks[0, 0, :] = 0
+        got = bwd(q, k, v, g, masks, T, 0.55)
+        ref = _autograd_masked(q, k, v, g, masks, T, 0.55)
+        for a, r, name in zip(got, ref, "qkv"):
+            assert np.max(np.abs(a - r)) < 1e-11, f"d{name}"
+
+
+def pin_bwd_bruteforce(bwd):
+    """Pure-Python chain rule through the softmax, token by token."""
+    rng = np.random.default_rng(21)
+    F, T, d, scale = 3, 2, 3, 0.8
+    mask = np.array([[1, 0, 1], [0, 0, 0], [1, 1, 0]], np.uint8)
+    q, k, v, g = (_rand(rng, 1, 1, F * T, d, 0.7) for _ in range(4))
+    dq, dk, dv = bwd(q, k, v, g, mask, T, scale)
+    S = F * T
+    edq, edk, edv = np.zeros((S, d)), np.zeros((S, d)), np.zeros((S, d))
+    for s in range(S):
+        kept = [t for t in range(S) if mask[s // T][t // T]]
+        if not kept:
+            continue
+        w = {t: math.exp(scale * sum(q[0, 0, s, c] * k[0, 0, t, c] for c in range(d))) for t in kept}
+        z = sum(w.values())
+        p = {t: w[t] / z for t in kept}
+        out = [sum(p[t] * v[0, 0, t, c] for t in kept) for c in range(d)]
+        dp = {t: sum(g[0, 0, s, c] * v[0, 0, t, c] for c in range(d)) for t in kept}
+        big_d = sum(g[0, 0, s, c] * out[c] for c in range(d))
+        for t in kept:
+            ds = p[t] * (dp[t] - big_d)
+            for c in range(d):
+                edq[s, c] += scale * ds * k[0, 0, t, c]
+                edk[t, c] += scale * ds * q[0, 0, s, c]
+                edv[t, c] += p[t] * g[0, 0, s, c]
+    for a, e in ((dq, edq), (dk, edk), (dv, edv)):
+        assert np.max(np.abs(a[0, 0] - e)) < TOL
+
+
+def pin_bwd_uniform_weights(bwd):
+    """Q = 0: P is uniform over the kept keys, so dv_t = sum over the rows keeping t of
+    dO_s / n_s (n_s = kept keys of s) and dk = 0 (all scores equal, dS sums to zero
+    against equal q = 0)."""
+    rng = np.random.default_rng(22)
+    F, T, d = 4, 3, 5
+    mask = (rng.random((F, F)) < 0.5).astype(np.uint8)
+    mask[0, :] = 1
+    k, v, g = (_rand(rng, 1, 1, F * T, d) for _ in range(3))
+    dq, dk, dv = bwd(np.zeros_like(k), k, v, g, mask, T, 0.9)
+    assert np.max(np.abs(dk)) < TOL
+    expect = np.zeros((F * T, d))
+    for s in range(F * T):
+        kept = [t for t in range(F * T) if mask[s // T][t // T]]
+        for t in kept:
+            expect[t] += g[0, 0, s] / len(kept)
+    assert np.max(np.abs(dv[0, 0] - expect)) < TOL
+
+
+BWD_PINS = [pin_bwd_matches_autograd, pin_bwd_bruteforce, pin_bwd_uniform_weights]
