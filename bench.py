@@ -28,7 +28,7 @@ import workloads  # noqa: E402
 # MI355X dense bf16 matrix peak: 256 CUs x 4096 FLOP/clk x 2.4 GHz (the published 2.5 PFLOP/s).
 PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2502_06155_amd", "csrc", f)
-               for f in ("tile_attn_kernels.hip", "launch.h")]
+               for f in ("tile_attn_kernels.hip", "tile_common.h", "launch.h")]
 PROFILE_MD = os.path.join(ROOT, "profiles", "tile_attn_fwd_93f_col_g1.md")
 
 

@@ -102,6 +102,37 @@ int tile_attn_fwd_heads(const void* q, const void* k, const void* v, void* out,
                         float* lse, void* stream);
 
 /*
+ * Gradients of tile-sparse attention (the op the sparse student of Sec. 3.4 is
+ * trained through). With P[s,t] = exp(scale * <q[s], k[t]> - lse[s]) over the kept
+ * pairs, dP[s,t] = <dout[s], v[t]>, delta[s] = <dout[s], out[s]> and
+ * dS = P * (dP - delta):
+ *     dq[s] = scale * sum_t dS[s,t] k[t],  dk[t] = scale * sum_s dS[s,t] q[s],
+ *     dv[t] = sum_s P[s,t] dout[s],
+ * sums over kept pairs only: keys of frames no query frame keeps get zero dk and
+ * dv, queries of frames that keep nothing get zero dq. Dropped tiles are never
+ * read.
+ *
+ * q, k, v: the forward's inputs; out, lse: what tile_attn_fwd_heads returned for
+ *   them with the same masks and scale (out bf16 [B, H, S, d], lse fp32 [B, H, S],
+ *   DEVICE). dout: DEVICE bf16 [B, H, S, d], the gradient of out.
+ * dq, dk, dv: DEVICE bf16 [B, H, S, d] outputs, fully written (rounded to bf16,
+ *   RNE, from fp32 sums). They must not overlap each other or any input.
+ * tile_masks, n_masks: as for tile_attn_fwd_heads. All bf16 tensors 16-byte
+ *   aligned, lse 4-byte aligned.
+ * Workspace: B*H*S*8 bytes for the base-2 lse and delta, plus fp32 partials for
+ *   frames the plan splits (the query side plans the mask, the key side its
+ *   transpose, each as tile_attn_plan describes), held per (device, stream) like
+ *   the forward's.
+ * Errors: those of tile_attn_fwd_heads (TA_ERR_NULL_PTR also for out, dout, lse,
+ *   dq, dk, dv; TA_ERR_OVERLAP when an output overlaps an input or another
+ *   output).
+ */
+int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out,
+                  const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                  int B, int H, int F, int T, int d,
+                  const uint8_t* tile_masks, int n_masks, float scale, void* stream);
+
+/*
  * Dense control: 3D full attention (every tile kept, the "full" rows of
  * tab:kernel_time). Runs the same kernel as tile_attn_fwd with an all-ones
  * mask, so its output is bit-identical to tile_attn_fwd with that mask.

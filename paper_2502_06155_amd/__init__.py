@@ -1,4 +1,4 @@
-"""Tile-sparse 3D attention forward for MI355X (gfx950).
+"""Tile-sparse 3D attention (forward and gradients) for MI355X (gfx950).
 
 The hot path of Efficient-vDiT (arXiv 2502.06155): softmax attention in which
 each query latent frame only attends to the key frames its frame-tile mask
@@ -12,6 +12,7 @@ from .api import (  # noqa: F401
     dense_attn,
     dense_attn_fwd,
     tile_attn,
+    tile_attn_bwd,
     tile_attn_compact,
     tile_attn_fwd,
     tile_attn_fwd_heads,

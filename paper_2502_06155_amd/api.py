@@ -74,6 +74,20 @@ def tile_attn_fwd_heads(q, k, v, out, B: int, H: int, F: int, T: int, d: int, ti
                                    _stream(stream)), "tile_attn_fwd_heads")
 
 
+def tile_attn_bwd(q, k, v, out, dout, lse, dq, dk, dv, B: int, H: int, F: int, T: int,
+                  d: int, tile_masks, scale: float, stream=None) -> None:
+    """tile_attn_bwd of the C ABI: gradients dq, dk, dv (bf16 [B, H, F*T, d]) from the
+    forward's out and lse (fp32 [B, H, F*T]) and dout; tile_masks as for
+    tile_attn_fwd_heads."""
+    m = np.ascontiguousarray(np.asarray(tile_masks), dtype=np.uint8)
+    if m.size % (F * F):
+        raise ValueError("tile_masks must hold n_masks * F * F entries")
+    n_masks = m.size // (F * F)
+    _check(lib.tile_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+                             _ptr(dq), _ptr(dk), _ptr(dv), B, H, F, T, d, m.ctypes.data,
+                             n_masks, float(scale), _stream(stream)), "tile_attn_bwd")
+
+
 def dense_attn_fwd(q, k, v, out, B: int, H: int, F: int, T: int, d: int, scale: float,
                    stream=None) -> None:
     """dense_attn_fwd of the C ABI: every tile kept."""

@@ -47,4 +47,64 @@ struct MergeArgs {
 hipError_t launch_tile_attn_fwd(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_merge_partials(const MergeArgs& a, hipStream_t stream);
 
+// Gradients. The prep pass turns the forward's natural-log log-sum-exp into base 2
+// and forms delta = <dO, out> per query row.
+struct PrepArgs {
+  const uint16_t* out;
+  const uint16_t* dout;
+  const float* lse;  // natural log, [rows]
+  float* lse2;       // base 2, [rows]
+  float* delta;      // [rows]
+  int64_t rows;      // B * H * F * T
+  int d;
+};
+
+// The two gradient kernels. The query-side pass (dq) walks each query frame's kept
+// key frames with the forward's work list; the key-side pass (dk, dv) walks each
+// key frame's keeping query frames with the work list of the transposed mask.
+// Items are 5 int32 as in FwdArgs; split frames write fp32 partials [n_slots][B][T][d]
+// that sum_partials adds up.
+struct BwdArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const uint16_t* dout;
+  uint16_t* dq;
+  uint16_t* dk;
+  uint16_t* dv;
+  int B, H, F, T, d;
+  const float* lse2;
+  const float* delta;
+  const int32_t* items_q;
+  const int32_t* cols_q;
+  int n_items_q;
+  float* ws_dq;
+  const int32_t* items_k;
+  const int32_t* cols_k;
+  int n_items_k;
+  float* ws_dk;
+  float* ws_dv;
+  float c;           // > 0: |scale| * log2(e)
+  float scale;       // multiplies dq and dk
+  uint32_t flip;     // 0x80008000 flips the sign of the logits' q (dq pass) or k (dk/dv pass)
+  uint32_t keep;     // 0 zeroes that operand (scale 0), else ~0
+  uint32_t n_wg_q;   // B * n_items_q * ceil(T / 256)
+  uint32_t n_wg_k;   // B * n_items_k * ceil(T / bwd_keys_per_workgroup(d))
+};
+
+// Adds the partials of split frames: heavy holds {head, frame, first slot, slots}.
+struct SumArgs {
+  const float* ws;
+  const int32_t* heavy;
+  int n_heavy;
+  int B, H, F, T, d;
+  uint16_t* out;
+};
+
+int bwd_keys_per_workgroup(int d);
+hipError_t launch_bwd_prep(const PrepArgs& a, hipStream_t stream);
+hipError_t launch_bwd_dq(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_dkdv(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_sum_partials(const SumArgs& a, hipStream_t stream);
+
 }  // namespace ta

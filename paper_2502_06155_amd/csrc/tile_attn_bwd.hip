@@ -1,0 +1,643 @@
+// gfx950 (MI355X, CDNA4) kernels for the gradients of tile-sparse 3D attention.
+//
+// What is computed: the forward pass (Sec. 3.3 of Efficient-vDiT) gives query
+// token s the output out_s = sum_t P_st v_t, P_st = softmax over the keys t of the
+// frames its frame keeps of scale * <q_s, k_t>. With the upstream gradient dO, the
+// forward's row log-sum-exp lse_s and delta_s = <dO_s, out_s>, the chain rule
+// through the softmax gives, over kept (s, t) pairs only:
+//   P_st = exp(scale <q_s, k_t> - lse_s),  dP_st = <dO_s, v_t>,
+//   dS_st = P_st (dP_st - delta_s),
+//   dq_s = scale sum_t dS_st k_t,  dk_t = scale sum_s dS_st q_s,  dv_t = sum_s P_st dO_s.
+// Stage 3 of the method (Sec. 3.4) trains the sparse model through this; dropped
+// tiles are never read here either.
+//
+// Passes (all on the caller's stream)
+//   prep  lse in base 2 and delta per query row.
+//   dq    one workgroup per 256 query rows of a query frame, over the kept key
+//         tiles (the forward's work list): S^T = K Q^T, dP^T = V dO^T,
+//         dQ^T += K^T dS^T. Each lane owns one query of each of its two 32-query
+//         column blocks, so lse and delta are per-lane constants.
+//   dkdv  one workgroup per 256 key rows (128 for d = 128) of a key frame, over the
+//         query tiles of the frames that keep it (the work list of the transposed
+//         mask): S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dS. Each lane
+//         owns one key of each of its 32-key column blocks.
+//   sum   adds the fp32 partials of frames the work plan split into pieces.
+// dq is recomputed in its own pass instead of being accumulated from the key side:
+// fp32 atomics from every (key block, query block) pair would move several TB/s
+// through L2 at this shape, more than recomputing S and dP costs on the matrix cores.
+//
+// Both gradient kernels keep one operand of every product in registers (the
+// wave's 64 queries or 64 keys) and stream the other through LDS, so each fragment
+// read from LDS feeds two MFMAs, as in the forward kernel. With three register
+// operands and two accumulator sets per wave they run one workgroup (4 waves) per
+// CU, up to 512 registers per lane.
+//
+// LDS layout: every staged tile is read both row-wise (16 bytes per lane, 16
+// consecutive rows per access) and transposed (ds_read_b64_tr_b16: 4 consecutive
+// rows x 64 bytes per half-wave access), so one XOR swizzle dsw(r) of the 16-byte
+// pieces serves both: over 16 consecutive rows it spreads one piece column over
+// all 64 banks, and over 4 consecutive rows (starting at a multiple of 4) it puts
+// the rows' 64-byte quads in different bank groups.
+#include <hip/hip_runtime.h>
+
+#include <float.h>
+#include <stdint.h>
+
+#include "launch.h"
+#include "tile_common.h"
+
+namespace ta {
+namespace {
+
+constexpr int kBwdWaves = 4;
+constexpr int kBwdThreads = 64 * kBwdWaves;
+constexpr int kQRowsPerWg = 256;  // dq pass: 64 query rows per wave
+
+// 32-key blocks per wave in the dk/dv pass: two (64 keys) where the registers
+// allow it, one at d = 128.
+template <int D>
+constexpr int key_blocks() { return D <= 96 ? 2 : 1; }
+template <int D>
+constexpr int keys_per_wg() { return kBwdWaves * 32 * key_blocks<D>(); }
+
+template <int D>
+struct BShape {
+  static constexpr int kChunks = D / 16;
+  static constexpr int kDBlocks = D / 32;
+  static constexpr int kPieces = D / 8;
+  static constexpr int kTileElems = kBlockK * D;
+  static constexpr int kLoadsPerWave = kBlockK * kPieces / 64 / kBwdWaves;
+  static_assert(kBlockK * kPieces == 64 * kBwdWaves * kLoadsPerWave, "whole loads per wave");
+};
+
+template <int D>
+__device__ __forceinline__ int dsw(int r) {
+  if constexpr (D == 64) return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+  else if constexpr (D == 96) return (r >> 2) & 3;
+  else return ((r & 3) << 2) | ((r >> 2) & 3);
+}
+template <int D>
+__device__ __forceinline__ int d_slot(int r, int p) { return (r * (D / 8) + (p ^ dsw<D>(r))) * 8; }
+
+// Direct global -> LDS loads of one 64-row tile in the dsw layout (see the
+// forward kernel's TileLoader: the XOR only permutes pieces inside a row, and one
+// load covers whole rows or aligned quads, so it reads contiguous memory).
+template <int D>
+struct DualLoader {
+  int off[BShape<D>::kLoadsPerWave];
+  __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < BShape<D>::kLoadsPerWave; ++j) {
+      const int q = 64 * (wave + kBwdWaves * j) + lane;
+      const int r = q / BShape<D>::kPieces, ps = q % BShape<D>::kPieces;
+      off[j] = (r * D + 8 * (ps ^ dsw<D>(r))) * 2;
+    }
+  }
+  __device__ __forceinline__ void load(const uint16_t* Xh, size_t row0, int nvalid,
+                                       const uint16_t* lds, int wave) const {
+    const i32x4 rs = buffer_words(Xh + row0 * D, (uint32_t)(nvalid * D * 2));
+    const uint32_t base = lds_addr(lds);
+#pragma unroll
+    for (int j = 0; j < BShape<D>::kLoadsPerWave; ++j)
+      load_to_lds(rs, __builtin_amdgcn_readfirstlane(base + 1024u * (uint32_t)(wave + kBwdWaves * j)),
+                  off[j]);
+  }
+};
+
+// Row-wise fragment offsets (A operand, rows = tile rows): lane (n, h) reads row
+// n of a 32-row block, piece 2 cc + h of chunk cc. Row block rb adds rb * 32 * D
+// (the swizzle depends only on the low 4 bits of the row).
+template <int D>
+struct RowAddr {
+  int at[D / 16];
+  __device__ __forceinline__ void init(int n, int hf) {
+#pragma unroll
+    for (int cc = 0; cc < D / 16; ++cc) at[cc] = d_slot<D>(n, 2 * cc + hf);
+  }
+};
+
+// Transposed fragment offsets (A operand, rows = d, contraction over tile rows):
+// lane l (group g = l/16, j = l%16) reads row 4(g/2) + j/4 (lo) and that row + 8
+// (hi), d = 32 mb + 16(g%2) + 4(j%4) .. +3. Chunk ch (16 rows) adds 16 ch * D.
+template <int D>
+struct TrAddr {
+  int lo[D / 32], hi[D / 32];
+  __device__ __forceinline__ void init(int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const int r = 4 * (g >> 1) + (j >> 2);
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb) {
+      const int p = 4 * mb + 2 * (g & 1) + ((j >> 1) & 1);
+      lo[mb] = d_slot<D>(r, p) + 4 * (j & 1);
+      hi[mb] = d_slot<D>(r + 8, p) + 4 * (j & 1);
+    }
+  }
+};
+
+template <int D>
+__device__ __forceinline__ bf16x8 row_frag(const uint16_t* tile, const RowAddr<D>& ra, int rb, int cc) {
+  return as_bf16x8(load16(tile + rb * 32 * D + ra.at[cc]));
+}
+
+// 32 d-rows x 16 tile rows: the contraction index k of lane half h maps to tile
+// rows 16 ch + 4h + (0..3) and 16 ch + 8 + 4h + (0..3), the order in which a C
+// fragment's entries 8c2 .. 8c2+7 hold their rows.
+template <int D>
+__device__ __forceinline__ bf16x8 tr_frag(const uint16_t* tile, const TrAddr<D>& ta, int mb, int ch) {
+  const uint16_t* p = tile + 16 * ch * D;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + ta.lo[mb]));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + ta.hi[mb]));
+  const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+  return as_bf16x8(u32x4{a[0], a[1], b[0], b[1]});
+}
+
+// B-operand slices of this lane's row (query or key) of a tensor: d = 16 cc + 8h .. +7.
+template <int D>
+__device__ __forceinline__ void load_row_operand(const uint16_t* row, bool valid, uint32_t keep,
+                                                 uint32_t flip, int hf, bf16x8 (&x)[D / 16]) {
+#pragma unroll
+  for (int cc = 0; cc < D / 16; ++cc) {
+    u32x4 w = {0u, 0u, 0u, 0u};
+    if (valid) w = (load16(row + 16 * cc + 8 * hf) & keep) ^ flip;
+    x[cc] = as_bf16x8(w);
+  }
+}
+
+// Stores 16 d-values of this lane's row from a transposed accumulator block
+// (entry 4i + j holds d = 32 mb + 8i + 4h + j), times s, as bf16 or fp32.
+template <int D>
+__device__ __forceinline__ void store_row_bf16(uint16_t* row, const f32x16 (&acc)[D / 32], float s, int hf) {
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f32x4 x = {acc[mb][4 * i] * s, acc[mb][4 * i + 1] * s, acc[mb][4 * i + 2] * s,
+                       acc[mb][4 * i + 3] * s};
+      const bf16x4 y = __builtin_convertvector(x, bf16x4);
+      *reinterpret_cast<u32x2*>(row + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
+    }
+}
+template <int D>
+__device__ __forceinline__ void store_row_f32(float* row, const f32x16 (&acc)[D / 32], float s, int hf) {
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f32x4 x = {acc[mb][4 * i] * s, acc[mb][4 * i + 1] * s, acc[mb][4 * i + 2] * s,
+                       acc[mb][4 * i + 3] * s};
+      *reinterpret_cast<f32x4*>(row + 32 * mb + 8 * i + 4 * hf) = x;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// prep: lse2 = lse * log2(e), delta = <dO, out> (fp32 sum of bf16 products).
+template <int D>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restrict__ out,
+                                                       const uint16_t* __restrict__ dout,
+                                                       const float* __restrict__ lse,
+                                                       float* __restrict__ lse2,
+                                                       float* __restrict__ delta, int64_t rows) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= rows) return;
+  const uint16_t* o = out + r * D;
+  const uint16_t* g = dout + r * D;
+  float acc = 0.f;
+#pragma unroll
+  for (int c = 0; c < D / 8; ++c) {
+    const bf16x8 x = as_bf16x8(load16(o + 8 * c));
+    const bf16x8 y = as_bf16x8(load16(g + 8 * c));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)x[e], (float)y[e], acc);
+  }
+  delta[r] = acc;
+  lse2[r] = lse[r] * 1.4426950408889634f;
+}
+
+// ---------------------------------------------------------------------------
+// dq pass.
+//
+// dS^T of one 32-key block for one column block, as the B operand of
+// dQ^T += K^T dS^T: entries 8c2 .. 8c2+7 of the C fragment.
+__device__ __forceinline__ void dq_scores(const f32x16& s, const f32x16& dp, float c, float lse2,
+                                          float dlt, bf16x8 (&ds)[2]) {
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    f32x8 x;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float p = fast_exp2(__builtin_fmaf(s[8 * c2 + e], c, -lse2));
+      x[e] = p * (dp[8 * c2 + e] - dlt);
+    }
+    ds[c2] = __builtin_convertvector(x, bf16x8);
+  }
+}
+
+// Keys of block kb past the tile's valid rows get -inf: P = 0.
+__device__ __forceinline__ void mask_keys(f32x16& s, int kb, int hf, int nvalid) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int key = kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
+    if (key >= nvalid) s[r] = -INFINITY;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a, int nqb) {
+  using Sh = BShape<D>;
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
+
+  const uint32_t work = xcd_remap(blockIdx.x, a.n_wg_q);
+  const uint32_t per_b = (uint32_t)a.n_items_q * (uint32_t)nqb;
+  const uint32_t b = work / per_b;
+  const uint32_t rem = work - b * per_b;
+  const int32_t* item = a.items_q + 5 * (rem / nqb);
+  const uint32_t bh = b * (uint32_t)a.H + (uint32_t)item[0];
+  const int frame = item[1], kbeg = item[2], n_kept = item[3], slot = item[4];
+  const int qb = (int)(rem % nqb);
+  const int T = a.T;
+
+  const size_t head_elems = (size_t)a.F * T * D;
+  const uint16_t* Kh = a.k + bh * head_elems;
+  const uint16_t* Vh = a.v + bh * head_elems;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int n = lane & 31, hf = lane >> 5;
+  const int qrow0 = qb * kQRowsPerWg + wave * 64 + n;
+  const bool wave_active = qb * kQRowsPerWg + wave * 64 < T;
+
+  bf16x8 qf[2][Sh::kChunks], gf[2][Sh::kChunks];
+  float lse2[2], dlt[2];
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs) {
+    const int qrow = qrow0 + 32 * qs;
+    const bool valid = qrow < T;
+    const size_t r = ((size_t)bh * a.F + frame) * T + qrow;
+    load_row_operand<D>(a.q + r * D, valid, a.keep, a.flip, hf, qf[qs]);
+    load_row_operand<D>(a.dout + r * D, valid, ~0u, 0u, hf, gf[qs]);
+    lse2[qs] = valid ? a.lse2[r] : 0.f;
+    dlt[qs] = valid ? a.delta[r] : 0.f;
+  }
+
+  f32x16 acc[2][Sh::kDBlocks];
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs)
+#pragma unroll
+    for (int mb = 0; mb < Sh::kDBlocks; ++mb) acc[qs][mb] = f32x16{};
+
+  const int tpf = (T + kBlockK - 1) / kBlockK;
+  const int n_tiles = n_kept * tpf;
+  if (n_tiles > 0) {
+    DualLoader<D> ld;
+    ld.init(wave, lane);
+    RowAddr<D> ra;
+    ra.init(n, hf);
+    TrAddr<D> ta;
+    ta.init(lane);
+    TileCursor cur, nxt;
+    cur.start(a.cols_q + kbeg, tpf, T);
+    ld.load(Kh, cur.key0(), cur.nvalid(), sK[0], wave);
+    ld.load(Vh, cur.key0(), cur.nvalid(), sV[0], wave);
+    nxt = cur;
+    nxt.advance(n_kept);
+    wait_tile_loads();
+    __syncthreads();
+
+    for (int t = 0; t < n_tiles; ++t) {
+      const int buf = t & 1;
+      if (t + 1 < n_tiles) {
+        ld.load(Kh, nxt.key0(), nxt.nvalid(), sK[buf ^ 1], wave);
+        ld.load(Vh, nxt.key0(), nxt.nvalid(), sV[buf ^ 1], wave);
+      }
+      const int nvalid = cur.nvalid();
+      if (wave_active) {
+        // One 32-key block at a time (not unrolled, which keeps the two blocks'
+        // fragments from being live together).
+#pragma unroll 1
+        for (int kb = 0; kb < 2; ++kb) {
+          f32x16 s[2], dp[2];
+          {
+            const bf16x8 k0 = row_frag<D>(sK[buf], ra, kb, 0);
+            const bf16x8 v0 = row_frag<D>(sV[buf], ra, kb, 0);
+            s[0] = mfma32(k0, qf[0][0], f32x16{});
+            s[1] = mfma32(k0, qf[1][0], f32x16{});
+            dp[0] = mfma32(v0, gf[0][0], f32x16{});
+            dp[1] = mfma32(v0, gf[1][0], f32x16{});
+          }
+#pragma unroll
+          for (int cc = 1; cc < Sh::kChunks; ++cc) {
+            const bf16x8 kx = row_frag<D>(sK[buf], ra, kb, cc);
+            const bf16x8 vx = row_frag<D>(sV[buf], ra, kb, cc);
+            s[0] = mfma32(kx, qf[0][cc], s[0]);
+            s[1] = mfma32(kx, qf[1][cc], s[1]);
+            dp[0] = mfma32(vx, gf[0][cc], dp[0]);
+            dp[1] = mfma32(vx, gf[1][cc], dp[1]);
+          }
+          if (nvalid < kBlockK) {
+            mask_keys(s[0], kb, hf, nvalid);
+            mask_keys(s[1], kb, hf, nvalid);
+          }
+          bf16x8 ds[2][2];
+          dq_scores(s[0], dp[0], a.c, lse2[0], dlt[0], ds[0]);
+          dq_scores(s[1], dp[1], a.c, lse2[1], dlt[1], ds[1]);
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+            for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
+              const bf16x8 kt = tr_frag<D>(sK[buf], ta, mb, 2 * kb + c2);
+              acc[0][mb] = mfma32(kt, ds[0][c2], acc[0][mb]);
+              acc[1][mb] = mfma32(kt, ds[1][c2], acc[1][mb]);
+            }
+        }
+      }
+      cur = nxt;
+      nxt.advance(n_kept);
+      wait_tile_loads();
+      __syncthreads();
+    }
+  }
+
+#pragma unroll
+  for (int qs = 0; qs < 2; ++qs) {
+    const int qrow = qrow0 + 32 * qs;
+    if (qrow >= T) continue;
+    if (slot < 0) {
+      store_row_bf16<D>(a.dq + (((size_t)bh * a.F + frame) * T + qrow) * D, acc[qs], a.scale, hf);
+    } else {
+      const size_t prow = ((size_t)slot * a.B + b) * T + qrow;
+      store_row_f32<D>(a.ws_dq + prow * D, acc[qs], a.scale, hf);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dk/dv pass.
+template <int D>
+__global__ __launch_bounds__(kBwdThreads, 1) void bwd_dkdv_kernel(const BwdArgs a, int nkb) {
+  using Sh = BShape<D>;
+  constexpr int KB = key_blocks<D>();
+  constexpr int kWgKeys = keys_per_wg<D>();
+  __shared__ __attribute__((aligned(1024))) uint16_t sQ[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sG[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(256))) float sL[2][kBlockK];
+  __shared__ __attribute__((aligned(256))) float sD[2][kBlockK];
+
+  const uint32_t work = xcd_remap(blockIdx.x, a.n_wg_k);
+  const uint32_t per_b = (uint32_t)a.n_items_k * (uint32_t)nkb;
+  const uint32_t b = work / per_b;
+  const uint32_t rem = work - b * per_b;
+  const int32_t* item = a.items_k + 5 * (rem / nkb);
+  const uint32_t bh = b * (uint32_t)a.H + (uint32_t)item[0];
+  const int frame = item[1], qbeg = item[2], n_keep = item[3], slot = item[4];
+  const int kblk = (int)(rem % nkb);
+  const int T = a.T;
+
+  const size_t head_rows = (size_t)a.F * T;
+  const uint16_t* Qh = a.q + bh * head_rows * D;
+  const uint16_t* Gh = a.dout + bh * head_rows * D;
+  const float* Lh = a.lse2 + bh * head_rows;
+  const float* Dh = a.delta + bh * head_rows;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int n = lane & 31, hf = lane >> 5;
+  const int krow0 = kblk * kWgKeys + wave * 32 * KB + n;
+  const bool wave_active = kblk * kWgKeys + wave * 32 * KB < T;
+
+  // This lane's keys (one per 32-key block) as B operands of S = Q K^T and
+  // dP = dO V^T.
+  bf16x8 kf[KB][Sh::kChunks], vf[KB][Sh::kChunks];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    const int krow = krow0 + 32 * kb;
+    const bool valid = krow < T;
+    const size_t r = ((size_t)bh * a.F + frame) * T + krow;
+    load_row_operand<D>(a.k + r * D, valid, a.keep, a.flip, hf, kf[kb]);
+    load_row_operand<D>(a.v + r * D, valid, ~0u, 0u, hf, vf[kb]);
+  }
+
+  f32x16 dk[KB][Sh::kDBlocks], dv[KB][Sh::kDBlocks];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+    for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
+      dk[kb][mb] = f32x16{};
+      dv[kb][mb] = f32x16{};
+    }
+
+  const int tpf = (T + kBlockK - 1) / kBlockK;
+  const int n_tiles = n_keep * tpf;
+  if (n_tiles > 0) {
+    DualLoader<D> ld;
+    ld.init(wave, lane);
+    RowAddr<D> ra;
+    ra.init(n, hf);
+    TrAddr<D> ta;
+    ta.init(lane);
+    auto load_tile = [&](const TileCursor& tc, int bi) {
+      const size_t row0 = tc.key0();
+      const int nv = tc.nvalid();
+      ld.load(Qh, row0, nv, sQ[bi], wave);
+      ld.load(Gh, row0, nv, sG[bi], wave);
+      if (wave == 0) {
+        load_dword_to_lds(buffer_words(Lh + row0, (uint32_t)(nv * 4)), lds_addr((const uint16_t*)sL[bi]),
+                          4 * lane);
+        load_dword_to_lds(buffer_words(Dh + row0, (uint32_t)(nv * 4)), lds_addr((const uint16_t*)sD[bi]),
+                          4 * lane);
+      }
+    };
+    TileCursor cur, nxt;
+    cur.start(a.cols_k + qbeg, tpf, T);
+    load_tile(cur, 0);
+    nxt = cur;
+    nxt.advance(n_keep);
+    wait_tile_loads();
+    __syncthreads();
+
+    for (int t = 0; t < n_tiles; ++t) {
+      const int buf = t & 1;
+      if (t + 1 < n_tiles) load_tile(nxt, buf ^ 1);
+      const int nvalid = cur.nvalid();
+      if (wave_active) {
+        // One 32-query half of the tile at a time (not unrolled: the halves would
+        // otherwise be interleaved past the register budget).
+#pragma unroll 1
+        for (int qc = 0; qc < 2; ++qc) {
+          f32x16 s[KB], dp[KB];
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) {
+            s[kb] = f32x16{};
+            dp[kb] = f32x16{};
+          }
+#pragma unroll
+          for (int cc = 0; cc < Sh::kChunks; ++cc) {
+            const bf16x8 qx = row_frag<D>(sQ[buf], ra, qc, cc);
+            const bf16x8 gx = row_frag<D>(sG[buf], ra, qc, cc);
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) {
+              s[kb] = mfma32(qx, kf[kb][cc], s[kb]);
+              dp[kb] = mfma32(gx, vf[kb][cc], dp[kb]);
+            }
+          }
+          if (nvalid < kBlockK) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int qr = 32 * qc + 8 * (e >> 2) + 4 * hf + (e & 3);
+              if (qr >= nvalid) {
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb) s[kb][e] = -INFINITY;
+              }
+            }
+          }
+          // Entry 8 c2 + 4 u + j holds query row 32 qc + 16 c2 + 8u + 4h + j.
+          bf16x8 pb[KB][2], db[KB][2];
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2) {
+            f32x4 l4[2], d4[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              l4[u] = *reinterpret_cast<const f32x4*>(&sL[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
+              d4[u] = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
+            }
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) {
+              f32x8 p8, d8;
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float p = fast_exp2(__builtin_fmaf(s[kb][8 * c2 + e], a.c, -l4[e >> 2][e & 3]));
+                p8[e] = p;
+                d8[e] = p * (dp[kb][8 * c2 + e] - d4[e >> 2][e & 3]);
+              }
+              pb[kb][c2] = __builtin_convertvector(p8, bf16x8);
+              db[kb][c2] = __builtin_convertvector(d8, bf16x8);
+            }
+          }
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+            for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
+              const bf16x8 gt = tr_frag<D>(sG[buf], ta, mb, 2 * qc + c2);
+              const bf16x8 qt = tr_frag<D>(sQ[buf], ta, mb, 2 * qc + c2);
+#pragma unroll
+              for (int kb = 0; kb < KB; ++kb) {
+                dv[kb][mb] = mfma32(gt, pb[kb][c2], dv[kb][mb]);
+                dk[kb][mb] = mfma32(qt, db[kb][c2], dk[kb][mb]);
+              }
+            }
+        }
+      }
+      cur = nxt;
+      nxt.advance(n_keep);
+      wait_tile_loads();
+      __syncthreads();
+    }
+  }
+
+  // dK uses the unflipped q of the LDS tiles, so scale (with its sign) applies.
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    const int krow = krow0 + 32 * kb;
+    if (krow >= T) continue;
+    if (slot < 0) {
+      const size_t r = ((size_t)bh * a.F + frame) * T + krow;
+      store_row_bf16<D>(a.dk + r * D, dk[kb], a.scale, hf);
+      store_row_bf16<D>(a.dv + r * D, dv[kb], 1.f, hf);
+    } else {
+      const size_t prow = ((size_t)slot * a.B + b) * T + krow;
+      store_row_f32<D>(a.ws_dk + prow * D, dk[kb], a.scale, hf);
+      store_row_f32<D>(a.ws_dv + prow * D, dv[kb], 1.f, hf);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Sum of the partials of split frames: one thread per (split frame, batch entry,
+// row, 8 consecutive d), rounded to bf16 (RNE).
+template <int D>
+__global__ __launch_bounds__(256) void sum_partials_kernel(const float* __restrict__ ws,
+                                                           const int32_t* __restrict__ heavy,
+                                                           int n_heavy, int B, int H, int F, int T,
+                                                           uint16_t* __restrict__ out) {
+  constexpr int kGroups = D / 8;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t per_frame = (size_t)B * T * kGroups;
+  if (idx >= per_frame * (size_t)n_heavy) return;
+  const int hv = (int)(idx / per_frame);
+  const size_t r = idx - (size_t)hv * per_frame;
+  const int grp = (int)(r % kGroups);
+  const size_t row = r / kGroups;  // b * T + t
+  const int head = heavy[4 * hv], frame = heavy[4 * hv + 1];
+  const int slot0 = heavy[4 * hv + 2], np = heavy[4 * hv + 3];
+  const size_t slot_stride = (size_t)B * T;
+  f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < np; ++p) {
+    const f32x4* src =
+        reinterpret_cast<const f32x4*>(ws + ((size_t)(slot0 + p) * slot_stride + row) * D + 8 * grp);
+    a0 += src[0];
+    a1 += src[1];
+  }
+  const size_t b = row / T, t = row - b * T;
+  const size_t orow = ((b * H + head) * F + frame) * (size_t)T + t;
+  const f32x8 x = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+  *reinterpret_cast<bf16x8*>(out + orow * D + 8 * grp) = __builtin_convertvector(x, bf16x8);
+}
+
+template <int D>
+hipError_t prep_d(const PrepArgs& a, hipStream_t stream) {
+  const int64_t blocks = (a.rows + 255) / 256;
+  hipLaunchKernelGGL(bwd_prep_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.out, a.dout,
+                     a.lse, a.lse2, a.delta, a.rows);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t dq_d(const BwdArgs& a, hipStream_t stream) {
+  const int nqb = (a.T + kQRowsPerWg - 1) / kQRowsPerWg;
+  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.n_wg_q), dim3(kBwdThreads), 0, stream, a, nqb);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t dkdv_d(const BwdArgs& a, hipStream_t stream) {
+  const int nkb = (a.T + keys_per_wg<D>() - 1) / keys_per_wg<D>();
+  hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream, a, nkb);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t sum_d(const SumArgs& a, hipStream_t stream) {
+  const size_t threads = (size_t)a.n_heavy * a.B * a.T * (D / 8);
+  const size_t blocks = (threads + 255) / 256;
+  hipLaunchKernelGGL(sum_partials_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.ws,
+                     a.heavy, a.n_heavy, a.B, a.H, a.F, a.T, a.out);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int bwd_keys_per_workgroup(int d) {
+  switch (d) {
+    case 64: return keys_per_wg<64>();
+    case 96: return keys_per_wg<96>();
+    case 128: return keys_per_wg<128>();
+    default: return 0;
+  }
+}
+
+#define TA_DISPATCH_D(fn, a, stream)          \
+  switch ((a).d) {                            \
+    case 64: return fn<64>(a, stream);        \
+    case 96: return fn<96>(a, stream);        \
+    case 128: return fn<128>(a, stream);      \
+    default: return hipErrorInvalidValue;     \
+  }
+
+hipError_t launch_bwd_prep(const PrepArgs& a, hipStream_t stream) { TA_DISPATCH_D(prep_d, a, stream) }
+hipError_t launch_bwd_dq(const BwdArgs& a, hipStream_t stream) { TA_DISPATCH_D(dq_d, a, stream) }
+hipError_t launch_bwd_dkdv(const BwdArgs& a, hipStream_t stream) { TA_DISPATCH_D(dkdv_d, a, stream) }
+hipError_t launch_sum_partials(const SumArgs& a, hipStream_t stream) { TA_DISPATCH_D(sum_d, a, stream) }
+
+#undef TA_DISPATCH_D
+
+}  // namespace ta

@@ -305,6 +305,133 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   return TA_OK;
 }
 
+
+// Gradients: prep (lse in base 2, delta), the query-side pass over the forward's
+// work list, the key-side pass over the work list of the transposed masks, and
+// the sums of split frames. The workspace holds [lse2][delta] (B*H*F*T floats
+// each), then the dq partials and the dk, dv partials.
+int run_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
+            const float* lse, void* dq, void* dk, void* dv, int B, int H, int F, int T, int d,
+            const uint8_t* masks, int n_masks, float scale, void* stream) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
+  const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
+  const int kpw = ta::bwd_keys_per_workgroup(d);
+  const int64_t nkb = (T + kpw - 1) / kpw;
+  const size_t part_row = (size_t)B * T * d * sizeof(float);
+
+  const DeviceWorkList* wq = nullptr;
+  int st = work_list_for(masks, n_masks, H, F, true, dev, &wq);
+  if (st != TA_OK) return st;
+  if ((size_t)wq->n_slots * part_row > kMaxWorkspaceBytes || (int64_t)B * wq->n_items * nqb > max_wg) {
+    st = work_list_for(masks, n_masks, H, F, false, dev, &wq);
+    if (st != TA_OK) return st;
+  }
+  std::vector<uint8_t> mt((size_t)n_masks * F * F);
+  for (int m = 0; m < n_masks; ++m)
+    for (int i = 0; i < F; ++i)
+      for (int j = 0; j < F; ++j)
+        mt[((size_t)m * F + i) * F + j] = masks[((size_t)m * F + j) * F + i];
+  const DeviceWorkList* wk = nullptr;
+  st = work_list_for(mt.data(), n_masks, H, F, true, dev, &wk);
+  if (st != TA_OK) return st;
+  if ((size_t)wk->n_slots * 2 * part_row > kMaxWorkspaceBytes || (int64_t)B * wk->n_items * nkb > max_wg) {
+    st = work_list_for(mt.data(), n_masks, H, F, false, dev, &wk);
+    if (st != TA_OK) return st;
+  }
+
+  const size_t rows = (size_t)B * H * F * T;
+  const size_t bytes = rows * 2 * sizeof(float) + (size_t)wq->n_slots * part_row +
+                       (size_t)wk->n_slots * 2 * part_row;
+  void* ws = nullptr;
+  st = workspace_for(dev, stream, bytes, &ws);
+  if (st != TA_OK) return st;
+  float* lse2 = static_cast<float*>(ws);
+  float* delta = lse2 + rows;
+  float* ws_dq = delta + rows;
+  float* ws_dk = ws_dq + (size_t)wq->n_slots * B * T * d;
+  float* ws_dv = ws_dk + (size_t)wk->n_slots * B * T * d;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+
+  ta::PrepArgs pa;
+  pa.out = static_cast<const uint16_t*>(out);
+  pa.dout = static_cast<const uint16_t*>(dout);
+  pa.lse = lse;
+  pa.lse2 = lse2;
+  pa.delta = delta;
+  pa.rows = (int64_t)rows;
+  pa.d = d;
+  e = ta::launch_bwd_prep(pa, s);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("prep launch: ") + hipGetErrorString(e));
+
+  ta::BwdArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.dout = static_cast<const uint16_t*>(dout);
+  a.dq = static_cast<uint16_t*>(dq);
+  a.dk = static_cast<uint16_t*>(dk);
+  a.dv = static_cast<uint16_t*>(dv);
+  a.B = B;
+  a.H = H;
+  a.F = F;
+  a.T = T;
+  a.d = d;
+  a.lse2 = lse2;
+  a.delta = delta;
+  a.items_q = wq->items;
+  a.cols_q = wq->cols;
+  a.n_items_q = wq->n_items;
+  a.ws_dq = ws_dq;
+  a.items_k = wk->items;
+  a.cols_k = wk->cols;
+  a.n_items_k = wk->n_items;
+  a.ws_dk = ws_dk;
+  a.ws_dv = ws_dv;
+  // As in the forward: the logits use |scale| with the sign folded into one
+  // operand (q in the dq pass, k in the dk/dv pass); scale 0 zeroes it.
+  if (scale == 0.f) {
+    a.c = 1.f;
+    a.flip = 0u;
+    a.keep = 0u;
+  } else {
+    a.c = std::max(std::fabs(scale) * 1.4426950408889634f, FLT_MIN);
+    a.flip = std::signbit(scale) ? 0x80008000u : 0u;
+    a.keep = 0xFFFFFFFFu;
+  }
+  a.scale = scale;
+  a.n_wg_q = (uint32_t)((int64_t)B * wq->n_items * nqb);
+  a.n_wg_k = (uint32_t)((int64_t)B * wk->n_items * nkb);
+  e = ta::launch_bwd_dq(a, s);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("dq launch: ") + hipGetErrorString(e));
+  e = ta::launch_bwd_dkdv(a, s);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("dk/dv launch: ") + hipGetErrorString(e));
+  auto sum = [&](const DeviceWorkList* wl, const float* part, void* dst, const char* what) -> int {
+    if (wl->n_heavy == 0) return TA_OK;
+    ta::SumArgs m;
+    m.ws = part;
+    m.heavy = wl->heavy;
+    m.n_heavy = wl->n_heavy;
+    m.B = B;
+    m.H = H;
+    m.F = F;
+    m.T = T;
+    m.d = d;
+    m.out = static_cast<uint16_t*>(dst);
+    hipError_t err = ta::launch_sum_partials(m, s);
+    if (err != hipSuccess)
+      return fail(TA_ERR_HIP, std::string(what) + " sum launch: " + hipGetErrorString(err));
+    return TA_OK;
+  };
+  if ((st = sum(wq, ws_dq, dq, "dq")) != TA_OK) return st;
+  if ((st = sum(wk, ws_dk, dk, "dk")) != TA_OK) return st;
+  if ((st = sum(wk, ws_dv, dv, "dv")) != TA_OK) return st;
+  g_last_error.clear();
+  return TA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -384,6 +511,39 @@ int dense_attn_fwd(const void* q, const void* k, const void* v, void* out, int B
   if (st != TA_OK) return st;
   std::vector<uint8_t> ones((size_t)F * F, 1);
   return run_fwd(q, k, v, out, B, H, F, T, d, ones.data(), 1, scale, nullptr, stream);
+}
+
+int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
+                  const float* lse, void* dq, void* dk, void* dv, int B, int H, int F, int T, int d,
+                  const uint8_t* tile_masks, int n_masks, float scale, void* stream) {
+  if (!out || !dout || !lse || !dq || !dk || !dv)
+    return fail(TA_ERR_NULL_PTR, "out, dout, lse, dq, dk and dv must be non-NULL");
+  int st = check_args(q, k, v, dq, B, H, F, T, d, scale);
+  if (st != TA_OK) return st;
+  if (!tile_masks) return fail(TA_ERR_NULL_PTR, "tile_masks must be non-NULL");
+  if (n_masks != 1 && n_masks != H) return fail(TA_ERR_BAD_MASK, "n_masks must be 1 or H");
+  for (const void* p : {out, dout, (const void*)dk, (const void*)dv})
+    if (reinterpret_cast<uintptr_t>(p) % 16)
+      return fail(TA_ERR_ALIGN, "q, k, v, out, dout, dq, dk and dv must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(lse) % 4) return fail(TA_ERR_ALIGN, "lse must be 4-byte aligned");
+  const int kpw = ta::bwd_keys_per_workgroup(d);
+  if ((int64_t)B * H * F * ((T + kpw - 1) / kpw) * ta::kThreads > (int64_t)UINT32_MAX)
+    return fail(TA_ERR_BAD_SHAPE, "the key-side pass would exceed the grid limit");
+  const size_t bytes = (size_t)B * H * F * T * d * 2;
+  const size_t lbytes = (size_t)B * H * F * T * sizeof(float);
+  const void* outs[3] = {dq, dk, dv};
+  for (int i = 0; i < 3; ++i) {
+    for (const void* p : {q, k, v, out, dout})
+      if (ranges_overlap(outs[i], bytes, p, bytes))
+        return fail(TA_ERR_OVERLAP, "dq, dk and dv must not overlap an input");
+    if (ranges_overlap(outs[i], bytes, lse, lbytes))
+      return fail(TA_ERR_OVERLAP, "dq, dk and dv must not overlap lse");
+    for (int j = i + 1; j < 3; ++j)
+      if (ranges_overlap(outs[i], bytes, outs[j], bytes))
+        return fail(TA_ERR_OVERLAP, "dq, dk and dv must not overlap each other");
+  }
+  return run_bwd(q, k, v, out, dout, lse, dq, dk, dv, B, H, F, T, d, tile_masks, n_masks, scale,
+                 stream);
 }
 
 const char* tile_attn_status_string(int status) {

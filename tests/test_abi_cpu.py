@@ -177,3 +177,29 @@ def test_heads_argument_errors_before_any_gpu_call():
     assert _heads(lse=(2 << 12) + 64) == 7  # lse overlaps k
     assert "overlap" in lib.tile_attn_last_error().decode()
     assert _heads(d=80) == 3 and _heads(B=0) == 2
+
+
+def _bwd(q=1 << 12, k=2 << 12, v=3 << 12, out=4 << 12, dout=5 << 12, lse=6 << 12, dq=7 << 12,
+         dk=8 << 12, dv=9 << 12, B=1, H=2, F=2, T=8, d=64, masks=None, n=None, scale=0.125):
+    m = np.ones((H, F, F), np.uint8) if masks is None else masks
+    nm = m.size // (F * F) if n is None else n
+    return lib.tile_attn_bwd(q, k, v, out, dout, lse, dq, dk, dv, B, H, F, T, d, m.ctypes.data, nm,
+                             scale, None)
+
+
+def test_bwd_argument_errors_before_any_gpu_call():
+    # every tensor of B=1, H=2, F=2, T=8, d=64 spans 4 KiB: the defaults are disjoint
+    assert _bwd(dout=None) == 1 and _bwd(lse=None) == 1 and _bwd(dv=None) == 1
+    assert lib.tile_attn_bwd(1 << 12, 2 << 12, 3 << 12, 4 << 12, 5 << 12, 6 << 12, 7 << 12,
+                             8 << 12, 9 << 12, 1, 2, 2, 8, 64, None, 2, 0.1, None) == 1
+    assert _bwd(n=3) == 4 and _bwd(n=0) == 4
+    assert _bwd(d=80) == 3 and _bwd(B=0) == 2 and _bwd(F=2000) == 2
+    assert _bwd(scale=float("inf")) == 6
+    assert _bwd(dk=(8 << 12) + 8) == 5 and _bwd(dout=(5 << 12) + 2) == 5
+    assert _bwd(lse=(6 << 12) + 2) == 5
+    assert _bwd(dq=(1 << 12) + 64) == 7  # dq overlaps q
+    assert _bwd(dk=(9 << 12) - 1024) == 7  # dk overlaps dv
+    assert "each other" in lib.tile_attn_last_error().decode()
+    assert _bwd(dv=(5 << 12) + 16) == 7  # dv overlaps dout
+    assert _bwd(lse=(7 << 12) + 64) == 7  # dq overlaps lse
+    assert "lse" in lib.tile_attn_last_error().decode()

@@ -3,6 +3,7 @@ planted mistakes that the pins must catch."""
 import importlib.util
 import os
 
+import numpy as np
 import pytest
 
 from oracle import backward as ob
@@ -45,3 +46,22 @@ def test_backward_pins_catch_planted_mistake(name, old, new):
         except Exception:
             failures += 1
     assert failures > 0, f"no pin caught: {name}"
+
+
+def test_rows_variant_matches_full_gradients():
+    """attention_backward_rows is the same computation restricted to chosen rows: it
+    must agree with the pinned attention_backward at every row, per-head masks, empty
+    rows and columns and several query chunks included."""
+    rng = np.random.default_rng(23)
+    B, H, F, T, d = 2, 2, 4, 7, 5
+    q, k, v, g = (rng.standard_normal((B, H, F * T, d)) for _ in range(4))
+    masks = (rng.random((H, F, F)) < 0.5).astype(np.uint8)
+    masks[0, 1, :] = 0
+    masks[1, :, 2] = 0
+    masks[1, 3, :] = 1
+    full = ob.attention_backward(q, k, v, g, masks, T, 0.4)
+    bb, hh, ss = np.meshgrid(np.arange(B), np.arange(H), np.arange(F * T), indexing="ij")
+    bb, hh, ss = bb.ravel(), hh.ravel(), ss.ravel()
+    dq, dk, dv = ob.attention_backward_rows(q, k, v, g, masks, T, 0.4, bb, hh, ss, bb, hh, ss, chunk=3)
+    for got, ref in zip((dq, dk, dv), full):
+        assert np.max(np.abs(got - ref[bb, hh, ss])) < 1e-12
