@@ -8,6 +8,12 @@ timed region), as in the paper's kernel benchmark.
 
 Prints ONE JSON line with the throughput over kept tiles, the roofline of the
 attention kernel, the dense control and the CPU oracle baseline.
+
+--pass bwd times the gradients instead: one step = one tile_attn_bwd call (prep,
+dq pass, dk/dv pass, sums of split frames) on the same problem, with out and the
+row log-sum-exp from one forward call made before the timed region. Its FLOP count
+is the usual five products per kept tile (S = QK^T, dP = dO V^T, dV = P^T dO,
+dK = dS^T Q, dQ = dS K): 10 * B * H * d * T^2 per kept tile.
 """
 from __future__ import annotations
 
@@ -27,18 +33,26 @@ import workloads  # noqa: E402
 
 # MI355X dense bf16 matrix peak: 256 CUs x 4096 FLOP/clk x 2.4 GHz (the published 2.5 PFLOP/s).
 PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12
-KERNEL_SRCS = [os.path.join(ROOT, "paper_2502_06155_amd", "csrc", f)
-               for f in ("tile_attn_kernels.hip", "tile_common.h", "launch.h")]
-PROFILE_MD = os.path.join(ROOT, "profiles", "tile_attn_fwd_93f_col_g1.md")
+CSRC = os.path.join(ROOT, "paper_2502_06155_amd", "csrc")
+KERNEL_SRCS = {
+    "fwd": [os.path.join(CSRC, f) for f in ("tile_attn_kernels.hip", "tile_common.h", "launch.h")],
+    "bwd": [os.path.join(CSRC, f) for f in ("tile_attn_bwd.hip", "tile_common.h", "launch.h")],
+}
+PROFILE_MD = {
+    "fwd": os.path.join(ROOT, "profiles", "tile_attn_fwd_93f_col_g1.md"),
+    "bwd": os.path.join(ROOT, "profiles", "tile_attn_bwd_93f_col_g1.md"),
+}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kept_flop(w, nnz: int) -> float:
-    """QK^T and PV over kept tiles only: 4 * B * H * d * T^2 per kept tile."""
-    return 4.0 * w.B * w.H * w.d * float(w.T) ** 2 * nnz
+def kept_flop(w, nnz: int, which: str = "fwd") -> float:
+    """Forward: QK^T and PV over kept tiles only, 4 * B * H * d * T^2 per kept tile.
+    Backward: the five products of the gradients, 10 * B * H * d * T^2 per kept tile."""
+    per = 4.0 if which == "fwd" else 10.0
+    return per * w.B * w.H * w.d * float(w.T) ** 2 * nnz
 
 
 def time_calls(fn, steps: int, warmup: int, torch):
@@ -67,19 +81,19 @@ def paper_stat(per_call):
     return float(np.median(a)), float(band.mean() if band.size else a.mean())
 
 
-def traffic_from_profile():
-    """HBM bytes per launch of the attention kernel from the committed rocprofv3
+def traffic_from_profile(which: str = "fwd"):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
     counter summary (FETCH_SIZE and WRITE_SIZE, each calibrated on a plain copy of
     known size), or None when the summary was taken on other kernel sources."""
-    if not os.path.exists(PROFILE_MD):
+    if not os.path.exists(PROFILE_MD[which]):
         return None
     rec = {}
-    with open(PROFILE_MD) as f:
+    with open(PROFILE_MD[which]) as f:
         for line in f:
             if ":" in line and not line.startswith(("|", "#", " ", "`")):
                 key, _, val = line.partition(":")
                 rec[key.strip()] = val.strip()
-    sha = hashlib.sha256(b"".join(open(p, "rb").read() for p in KERNEL_SRCS)).hexdigest()
+    sha = hashlib.sha256(b"".join(open(p, "rb").read() for p in KERNEL_SRCS[which])).hexdigest()
     if rec.get("kernel_sha256") != sha or "hbm_bytes_per_launch" not in rec:
         return None
     return float(rec["hbm_bytes_per_launch"])
@@ -112,6 +126,72 @@ def cpu_baseline(w, qb, kb, vb, mask, budget_s: float):
         "sample": f"float64 oracle on heads 0..{done - 1} of {w.H} (all {w.F} query frames, "
                   f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles",
     }
+
+
+def cpu_baseline_bwd(w, qb, kb, vb, gb, mask, budget_s: float):
+    """The float64 gradient oracle on whole heads of the same problem until the budget
+    is spent; kept TFLOP/s of that sample (five products per kept tile)."""
+    from oracle import backward as ob
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    nnz = int(np.count_nonzero(mask))
+    done, t0 = 0, time.perf_counter()
+    while done < w.H and time.perf_counter() - t0 < budget_s:
+        sl = slice(done, done + 1)
+        ob.attention_backward(qb[:, sl], kb[:, sl], vb[:, sl], gb[:, sl], mask, w.T, w.scale())
+        done += 1
+    dt = time.perf_counter() - t0
+    flop = 10.0 * w.B * done * w.d * float(w.T) ** 2 * nnz
+    return {
+        "value": flop / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"float64 gradient oracle on heads 0..{done - 1} of {w.H} (all {w.F} frames, "
+                  f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles",
+    }
+
+
+def make_grad_bits(w, seed: int = 1):
+    """Upstream gradient dO: N(0, 1) per element as bf16 bits, one PCG64 stream."""
+    rng = np.random.default_rng(seed)
+    return workloads.f32_to_bf16_bits(
+        rng.standard_normal((w.B, w.H, w.F * w.T, w.d), dtype=np.float32))
+
+
+class Problem:
+    """Device tensors of one workload and a step closure for one mask and pass."""
+
+    def __init__(self, torch, ta, w, qb, kb, vb, which: str):
+        self.torch, self.ta, self.w, self.which = torch, ta, w, which
+
+        def dev(x):
+            return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
+
+        self.q, self.k, self.v = dev(qb), dev(kb), dev(vb)
+        self.out = torch.empty_like(self.q)
+        if which == "bwd":
+            self.gb = make_grad_bits(w)
+            self.dout = dev(self.gb)
+            self.lse = torch.empty((w.B, w.H, w.F * w.T), dtype=torch.float32, device="cuda")
+            self.grads = [torch.empty_like(self.q) for _ in range(3)]
+        self.stream = torch.cuda.current_stream()
+
+    def step_fn(self, mask):
+        w, ta, st = self.w, self.ta, self.stream
+        q, k, v, out = self.q, self.k, self.v, self.out
+        if self.which == "fwd":
+            return lambda: ta.tile_attn_fwd(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), st)
+        # out and lse of this mask, once, outside the timed region
+        ta.tile_attn_fwd_heads(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), self.lse, st)
+        dq, dk, dv = self.grads
+        return lambda: ta.tile_attn_bwd(q, k, v, out, self.dout, self.lse, dq, dk, dv, w.B, w.H, w.F,
+                                        w.T, w.d, mask, w.scale(), st)
 
 
 def gemm_reference(torch, n: int = 16384, reps: int = 5):
@@ -158,31 +238,24 @@ def run_all(args, torch, ta):
         order += [c for c in ALL_CASES if c[0] == wname] + [(wname, "dense", 0)]
     for name, form, g in order:
         w = workloads.WORKLOADS[name]
-        if cur is None or cur[0] != name:
+        if cur is None or cur.w.name != name:
+            cur = None
             qb, kb, vb = workloads.make_workload_qkv(w)
-            dev = [torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda() for x in (qb, kb, vb)]
+            cur = Problem(torch, ta, w, qb, kb, vb, args.pass_)
             del qb, kb, vb
-            out = torch.empty_like(dev[0])
-            cur = (name, dev, out)
-        q, k, v = cur[1]
-        out = cur[2]
         mask = ta.tile_attn_make_mask(w.F, g, form)
         nnz = int(np.count_nonzero(mask))
-        stream = torch.cuda.current_stream()
-
-        def step():
-            ta.tile_attn_fwd(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), stream)
-
+        step = cur.step_fn(mask)
         steps = max(3, min(args.steps, int(2000 / max(1.0, nnz))))
         total, per = time_calls(step, steps, 2, torch)
         ms = total / steps
-        tf = kept_flop(w, nnz) / (ms * 1e-3) / 1e12
+        tf = kept_flop(w, nnz, args.pass_) / (ms * 1e-3) / 1e12
         if form == "dense":
             dense_ms[name] = ms
         row = {"workload": name, "form": form, "g": g, "nnz": nnz, "tiles": w.F * w.F, "ms": ms,
                "tflops": tf, "pct_peak": 100.0 * tf / PEAK_BF16_TFLOPS}
         rows.append(row)
-        log(f"[all] {name:8s} {form:5s} g={g} nnz {nnz:4d}/{w.F * w.F:<4d} {ms:9.3f} ms "
+        log(f"[all] {args.pass_} {name:8s} {form:5s} g={g} nnz {nnz:4d}/{w.F * w.F:<4d} {ms:9.3f} ms "
             f"{tf:7.1f} TFLOP/s ({row['pct_peak']:.1f}% of peak)")
     for row in rows:
         if row["workload"] in dense_ms and row["form"] != "dense":
@@ -199,6 +272,8 @@ def main():
     ap.add_argument("--workload", default="93f", choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--form", default="col", choices=["col", "sym", "dense"])
     ap.add_argument("--g", type=int, default=None)
+    ap.add_argument("--pass", dest="pass_", default="fwd", choices=["fwd", "bwd"],
+                    help="fwd: the attention forward (headline); bwd: its gradients")
     ap.add_argument("--dense-steps", type=int, default=5)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -233,35 +308,28 @@ def main():
 
     if args.all:
         rows = run_all(args, torch, ta)
-        print(json.dumps({"metric": "per-case ms/call and TFLOP/s over kept tiles", "unit": "TFLOP/s",
+        print(json.dumps({"metric": f"per-case ms/call and TFLOP/s over kept tiles ({args.pass_})",
+                          "unit": "TFLOP/s",
                           "n_gpus": 1, "dtype": "bf16", "data": "synthetic", "rows": rows}), flush=True)
         return
 
     w = workloads.WORKLOADS[args.workload]
     g = w.g if args.g is None else args.g
-    log(f"[bench] workload {w} form={args.form} g={g}")
+    which = args.pass_
+    log(f"[bench] workload {w} form={args.form} g={g} pass={which}")
     qb, kb, vb = workloads.make_workload_qkv(w)
     mask = ta.tile_attn_make_mask(w.F, g, args.form)
     nnz = int(np.count_nonzero(mask))
-
-    def dev(x):
-        return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
-
-    q, k, v = dev(qb), dev(kb), dev(vb)
-    out = torch.empty_like(q)
-    stream = torch.cuda.current_stream()
-    scale = w.scale()
-
-    def step():
-        ta.tile_attn_fwd(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, scale, stream)
+    prob = Problem(torch, ta, w, qb, kb, vb, which)
+    step = prob.step_fn(mask)
 
     torch.cuda.synchronize()
     total_ms, per = time_calls(step, args.steps, args.warmup, torch)
     ms = total_ms / args.steps
     med, band = paper_stat(per)
-    flop = kept_flop(w, nnz)
+    flop = kept_flop(w, nnz, which)
     tflops = flop / (ms * 1e-3) / 1e12
-    log(f"[bench] sparse: {ms:.3f} ms/call (median {med:.3f}, P20-P80 {band:.3f}), "
+    log(f"[bench] sparse {which}: {ms:.3f} ms/call (median {med:.3f}, P20-P80 {band:.3f}), "
         f"{tflops:.1f} TFLOP/s kept, nnz {nnz}/{w.F * w.F}")
 
     if args.profile_pass:
@@ -277,12 +345,10 @@ def main():
 
     extra = {}
     if not args.no_dense:
-        def dstep():
-            ta.dense_attn_fwd(q, k, v, out, w.B, w.H, w.F, w.T, w.d, scale, stream)
-
+        dstep = prob.step_fn(np.ones((w.F, w.F), np.uint8))
         dtot, dper = time_calls(dstep, args.dense_steps, 2, torch)
         dms = dtot / args.dense_steps
-        dflop = kept_flop(w, w.F * w.F)
+        dflop = kept_flop(w, w.F * w.F, which)
         extra = {
             "dense_ms_per_call": dms,
             "dense_tflops": dflop / (dms * 1e-3) / 1e12,
@@ -290,7 +356,7 @@ def main():
             "ideal_speedup": w.F * w.F / nnz,
         }
         extra["proportionality"] = tflops / extra["dense_tflops"]
-        log(f"[bench] dense: {dms:.3f} ms/call, {extra['dense_tflops']:.1f} TFLOP/s, "
+        log(f"[bench] dense {which}: {dms:.3f} ms/call, {extra['dense_tflops']:.1f} TFLOP/s, "
             f"speedup {extra['speedup_vs_dense']:.2f}x of ideal {extra['ideal_speedup']:.2f}x")
 
     gemm = None
@@ -300,12 +366,19 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, qb, kb, vb, mask, args.cpu_budget)
+        if which == "fwd":
+            cpu = cpu_baseline(w, qb, kb, vb, mask, args.cpu_budget)
+        else:
+            cpu = cpu_baseline_bwd(w, qb, kb, vb, prob.gb, mask, args.cpu_budget)
         log(f"[bench] cpu oracle: {cpu}")
 
     achieved = flop / (np.mean(per) * 1e-3) / 1e12
+    metric = "ms/call + effective TFLOP/s (kept tiles) and % bf16 MFMA peak, 24f×3600 tok"
+    if which == "bwd":
+        metric = ("backward ms/call + effective TFLOP/s (kept tiles, five products) and % bf16 "
+                  "MFMA peak, 24f×3600 tok")
     line = {
-        "metric": "ms/call + effective TFLOP/s (kept tiles) and % bf16 MFMA peak, 24f×3600 tok",
+        "metric": metric,
         "value": tflops,
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -323,6 +396,7 @@ def main():
         "config": {
             "workload": f"{w.name}: B={w.B} H={w.H} F={w.F} T={w.T} d={w.d}, "
                         f"{args.form} mask g={g} (nnz {nnz}/{w.F * w.F}), {w.dist} N(0,1) bf16 seed {w.seed}",
+            "pass": which,
             "kept_flop": flop,
             "nnz": nnz,
         },
@@ -332,7 +406,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": traffic_from_profile(),
+            "traffic": traffic_from_profile(which),
         },
         "cpu_baseline": cpu,
         "gemm_reference": gemm,

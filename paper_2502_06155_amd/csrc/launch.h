@@ -88,7 +88,7 @@ struct BwdArgs {
   float scale;       // multiplies dq and dk
   uint32_t flip;     // 0x80008000 flips the sign of the logits' q (dq pass) or k (dk/dv pass)
   uint32_t keep;     // 0 zeroes that operand (scale 0), else ~0
-  uint32_t n_wg_q;   // B * n_items_q * ceil(T / 256)
+  uint32_t n_wg_q;   // B * n_items_q * ceil(T / bwd_queries_per_workgroup(d))
   uint32_t n_wg_k;   // B * n_items_k * ceil(T / bwd_keys_per_workgroup(d))
 };
 
@@ -101,6 +101,7 @@ struct SumArgs {
   uint16_t* out;
 };
 
+int bwd_queries_per_workgroup(int d);
 int bwd_keys_per_workgroup(int d);
 hipError_t launch_bwd_prep(const PrepArgs& a, hipStream_t stream);
 hipError_t launch_bwd_dq(const BwdArgs& a, hipStream_t stream);

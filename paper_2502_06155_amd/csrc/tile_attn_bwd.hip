@@ -13,24 +13,22 @@
 //
 // Passes (all on the caller's stream)
 //   prep  lse in base 2 and delta per query row.
-//   dq    one workgroup per 256 query rows of a query frame, over the kept key
+//   dq    one workgroup per 128 query rows of a query frame, over the kept key
 //         tiles (the forward's work list): S^T = K Q^T, dP^T = V dO^T,
-//         dQ^T += K^T dS^T. Each lane owns one query of each of its two 32-query
-//         column blocks, so lse and delta are per-lane constants.
-//   dkdv  one workgroup per 256 key rows (128 for d = 128) of a key frame, over the
-//         query tiles of the frames that keep it (the work list of the transposed
-//         mask): S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dS. Each lane
-//         owns one key of each of its 32-key column blocks.
+//         dQ^T += K^T dS^T. Each lane owns one query of its wave's 32-query
+//         column block, so lse and delta are per-lane constants.
+//   dkdv  one workgroup per 128 key rows of a key frame, over the query tiles of
+//         the frames that keep it (the work list of the transposed mask):
+//         S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dS. Each lane owns
+//         one key of its wave's 32-key column block.
 //   sum   adds the fp32 partials of frames the work plan split into pieces.
 // dq is recomputed in its own pass instead of being accumulated from the key side:
 // fp32 atomics from every (key block, query block) pair would move several TB/s
 // through L2 at this shape, more than recomputing S and dP costs on the matrix cores.
 //
 // Both gradient kernels keep one operand of every product in registers (the
-// wave's 64 queries or 64 keys) and stream the other through LDS, so each fragment
-// read from LDS feeds two MFMAs, as in the forward kernel. With three register
-// operands and two accumulator sets per wave they run one workgroup (4 waves) per
-// CU, up to 512 registers per lane.
+// wave's 32 queries or 32 keys) and stream the other through LDS (see q_blocks
+// below for why not 64 as in the forward kernel).
 //
 // LDS layout: every staged tile is read both row-wise (16 bytes per lane, 16
 // consecutive rows per access) and transposed (ds_read_b64_tr_b16: 4 consecutive
@@ -51,12 +49,24 @@ namespace {
 
 constexpr int kBwdWaves = 4;
 constexpr int kBwdThreads = 64 * kBwdWaves;
-constexpr int kQRowsPerWg = 256;  // dq pass: 64 query rows per wave
-
-// 32-key blocks per wave in the dk/dv pass: two (64 keys) where the registers
-// allow it, one at d = 128.
+// Rows per wave, as 32-row column blocks: query blocks in the dq pass, key blocks
+// in the dk/dv pass. One block per wave keeps every operand, accumulator and score
+// in 256 VGPRs, so two workgroups share a CU and one wave's softmax-gradient
+// arithmetic overlaps the other's matrix instructions; measured at the 93-frame
+// shape this beats two blocks per wave at one workgroup per CU (which halves the
+// LDS fragment reads per MFMA but puts the accumulators in AGPRs and serialises
+// the vector work) by 17% (dq) and 12% (dk/dv). At d = 128 the dk/dv pass needs
+// more than 256 registers and runs one workgroup per CU.
 template <int D>
-constexpr int key_blocks() { return D <= 96 ? 2 : 1; }
+constexpr int q_blocks() { return 1; }
+template <int D>
+constexpr int key_blocks() { return 1; }
+template <int D>
+constexpr int dq_occupancy() { return q_blocks<D>() == 2 ? 1 : 2; }
+template <int D>
+constexpr int dkdv_occupancy() { return key_blocks<D>() == 2 || D == 128 ? 1 : 2; }
+template <int D>
+constexpr int queries_per_wg() { return kBwdWaves * 32 * q_blocks<D>(); }
 template <int D>
 constexpr int keys_per_wg() { return kBwdWaves * 32 * key_blocks<D>(); }
 
@@ -191,26 +201,45 @@ __device__ __forceinline__ void store_row_f32(float* row, const f32x16 (&acc)[D 
 
 // ---------------------------------------------------------------------------
 // prep: lse2 = lse * log2(e), delta = <dO, out> (fp32 sum of bf16 products).
+// One workgroup per 64 rows: the 256 threads read the rows' 16-byte pieces
+// contiguously (coalesced), leave per-piece partial dots in LDS, and 64 threads
+// add up one row each.
+constexpr int kPrepRows = 64;
+
 template <int D>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restrict__ out,
                                                        const uint16_t* __restrict__ dout,
                                                        const float* __restrict__ lse,
                                                        float* __restrict__ lse2,
                                                        float* __restrict__ delta, int64_t rows) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= rows) return;
-  const uint16_t* o = out + r * D;
-  const uint16_t* g = dout + r * D;
-  float acc = 0.f;
+  constexpr int kPieces = D / 8;
+  constexpr int kPerThread = kPrepRows * kPieces / 256;
+  static_assert(kPrepRows * kPieces == 256 * kPerThread, "whole pieces per thread");
+  __shared__ float part[kPrepRows * kPieces];
+  const int64_t row0 = (int64_t)blockIdx.x * kPrepRows;
+  const int64_t n_rows = rows - row0 < kPrepRows ? rows - row0 : kPrepRows;
+  const int64_t base = row0 * D;
 #pragma unroll
-  for (int c = 0; c < D / 8; ++c) {
-    const bf16x8 x = as_bf16x8(load16(o + 8 * c));
-    const bf16x8 y = as_bf16x8(load16(g + 8 * c));
+  for (int j = 0; j < kPerThread; ++j) {
+    const int piece = threadIdx.x + 256 * j;  // piece / kPieces = row within the block
+    float acc = 0.f;
+    if (piece < n_rows * kPieces) {
+      const bf16x8 x = as_bf16x8(load16(out + base + 8 * piece));
+      const bf16x8 y = as_bf16x8(load16(dout + base + 8 * piece));
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)x[e], (float)y[e], acc);
+      for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)x[e], (float)y[e], acc);
+    }
+    part[piece] = acc;
   }
-  delta[r] = acc;
-  lse2[r] = lse[r] * 1.4426950408889634f;
+  __syncthreads();
+  if (threadIdx.x < n_rows) {
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < kPieces; ++c) acc += part[threadIdx.x * kPieces + c];
+    const int64_t r = row0 + threadIdx.x;
+    delta[r] = acc;
+    lse2[r] = lse[r] * 1.4426950408889634f;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -242,8 +271,12 @@ __device__ __forceinline__ void mask_keys(f32x16& s, int kb, int hf, int nvalid)
 }
 
 template <int D>
-__global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a, int nqb) {
+__global__ __launch_bounds__(kBwdThreads, dq_occupancy<D>()) void bwd_dq_kernel(const BwdArgs a,
+                                                                                 int nqb) {
   using Sh = BShape<D>;
+  constexpr int QB = q_blocks<D>();
+  constexpr int kWaveRows = 32 * QB;
+  constexpr int kWgRows = kBwdWaves * kWaveRows;
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
 
@@ -264,13 +297,13 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a,
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hf = lane >> 5;
-  const int qrow0 = qb * kQRowsPerWg + wave * 64 + n;
-  const bool wave_active = qb * kQRowsPerWg + wave * 64 < T;
+  const int qrow0 = qb * kWgRows + wave * kWaveRows + n;
+  const bool wave_active = qb * kWgRows + wave * kWaveRows < T;
 
-  bf16x8 qf[2][Sh::kChunks], gf[2][Sh::kChunks];
-  float lse2[2], dlt[2];
+  bf16x8 qf[QB][Sh::kChunks], gf[QB][Sh::kChunks];
+  float lse2[QB], dlt[QB];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < QB; ++qs) {
     const int qrow = qrow0 + 32 * qs;
     const bool valid = qrow < T;
     const size_t r = ((size_t)bh * a.F + frame) * T + qrow;
@@ -280,9 +313,9 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a,
     dlt[qs] = valid ? a.delta[r] : 0.f;
   }
 
-  f32x16 acc[2][Sh::kDBlocks];
+  f32x16 acc[QB][Sh::kDBlocks];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs)
+  for (int qs = 0; qs < QB; ++qs)
 #pragma unroll
     for (int mb = 0; mb < Sh::kDBlocks; ++mb) acc[qs][mb] = f32x16{};
 
@@ -304,6 +337,42 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a,
     wait_tile_loads();
     __syncthreads();
 
+    // One 32-key block of the tile: S^T and dP^T for the wave's column blocks, the
+    // weights' gradient dS^T, then dQ^T += K^T dS^T.
+    auto key_block = [&](const uint16_t* tk, const uint16_t* tv, int kb, int nvalid) {
+      f32x16 s[QB], dp[QB];
+#pragma unroll
+      for (int qs = 0; qs < QB; ++qs) {
+        s[qs] = f32x16{};
+        dp[qs] = f32x16{};
+      }
+#pragma unroll
+      for (int cc = 0; cc < Sh::kChunks; ++cc) {
+        const bf16x8 kx = row_frag<D>(tk, ra, kb, cc);
+        const bf16x8 vx = row_frag<D>(tv, ra, kb, cc);
+#pragma unroll
+        for (int qs = 0; qs < QB; ++qs) {
+          s[qs] = mfma32(kx, qf[qs][cc], s[qs]);
+          dp[qs] = mfma32(vx, gf[qs][cc], dp[qs]);
+        }
+      }
+      if (nvalid < kBlockK) {
+#pragma unroll
+        for (int qs = 0; qs < QB; ++qs) mask_keys(s[qs], kb, hf, nvalid);
+      }
+      bf16x8 ds[QB][2];
+#pragma unroll
+      for (int qs = 0; qs < QB; ++qs) dq_scores(s[qs], dp[qs], a.c, lse2[qs], dlt[qs], ds[qs]);
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+        for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
+          const bf16x8 kt = tr_frag<D>(tk, ta, mb, 2 * kb + c2);
+#pragma unroll
+          for (int qs = 0; qs < QB; ++qs) acc[qs][mb] = mfma32(kt, ds[qs][c2], acc[qs][mb]);
+        }
+    };
+
     for (int t = 0; t < n_tiles; ++t) {
       const int buf = t & 1;
       if (t + 1 < n_tiles) {
@@ -312,43 +381,13 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a,
       }
       const int nvalid = cur.nvalid();
       if (wave_active) {
-        // One 32-key block at a time (not unrolled, which keeps the two blocks'
-        // fragments from being live together).
+        if constexpr (QB == 2) {
+          // Not unrolled: the two blocks' fragments would not fit the registers together.
 #pragma unroll 1
-        for (int kb = 0; kb < 2; ++kb) {
-          f32x16 s[2], dp[2];
-          {
-            const bf16x8 k0 = row_frag<D>(sK[buf], ra, kb, 0);
-            const bf16x8 v0 = row_frag<D>(sV[buf], ra, kb, 0);
-            s[0] = mfma32(k0, qf[0][0], f32x16{});
-            s[1] = mfma32(k0, qf[1][0], f32x16{});
-            dp[0] = mfma32(v0, gf[0][0], f32x16{});
-            dp[1] = mfma32(v0, gf[1][0], f32x16{});
-          }
-#pragma unroll
-          for (int cc = 1; cc < Sh::kChunks; ++cc) {
-            const bf16x8 kx = row_frag<D>(sK[buf], ra, kb, cc);
-            const bf16x8 vx = row_frag<D>(sV[buf], ra, kb, cc);
-            s[0] = mfma32(kx, qf[0][cc], s[0]);
-            s[1] = mfma32(kx, qf[1][cc], s[1]);
-            dp[0] = mfma32(vx, gf[0][cc], dp[0]);
-            dp[1] = mfma32(vx, gf[1][cc], dp[1]);
-          }
-          if (nvalid < kBlockK) {
-            mask_keys(s[0], kb, hf, nvalid);
-            mask_keys(s[1], kb, hf, nvalid);
-          }
-          bf16x8 ds[2][2];
-          dq_scores(s[0], dp[0], a.c, lse2[0], dlt[0], ds[0]);
-          dq_scores(s[1], dp[1], a.c, lse2[1], dlt[1], ds[1]);
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-            for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
-              const bf16x8 kt = tr_frag<D>(sK[buf], ta, mb, 2 * kb + c2);
-              acc[0][mb] = mfma32(kt, ds[0][c2], acc[0][mb]);
-              acc[1][mb] = mfma32(kt, ds[1][c2], acc[1][mb]);
-            }
+          for (int kb = 0; kb < 2; ++kb) key_block(sK[buf], sV[buf], kb, nvalid);
+        } else {
+          key_block(sK[buf], sV[buf], 0, nvalid);
+          key_block(sK[buf], sV[buf], 1, nvalid);
         }
       }
       cur = nxt;
@@ -359,7 +398,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a,
   }
 
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < QB; ++qs) {
     const int qrow = qrow0 + 32 * qs;
     if (qrow >= T) continue;
     if (slot < 0) {
@@ -374,7 +413,8 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_dq_kernel(const BwdArgs a,
 // ---------------------------------------------------------------------------
 // dk/dv pass.
 template <int D>
-__global__ __launch_bounds__(kBwdThreads, 1) void bwd_dkdv_kernel(const BwdArgs a, int nkb) {
+__global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_kernel(const BwdArgs a,
+                                                                                     int nkb) {
   using Sh = BShape<D>;
   constexpr int KB = key_blocks<D>();
   constexpr int kWgKeys = keys_per_wg<D>();
@@ -585,7 +625,7 @@ __global__ __launch_bounds__(256) void sum_partials_kernel(const float* __restri
 
 template <int D>
 hipError_t prep_d(const PrepArgs& a, hipStream_t stream) {
-  const int64_t blocks = (a.rows + 255) / 256;
+  const int64_t blocks = (a.rows + kPrepRows - 1) / kPrepRows;
   hipLaunchKernelGGL(bwd_prep_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.out, a.dout,
                      a.lse, a.lse2, a.delta, a.rows);
   return hipGetLastError();
@@ -593,7 +633,7 @@ hipError_t prep_d(const PrepArgs& a, hipStream_t stream) {
 
 template <int D>
 hipError_t dq_d(const BwdArgs& a, hipStream_t stream) {
-  const int nqb = (a.T + kQRowsPerWg - 1) / kQRowsPerWg;
+  const int nqb = (a.T + queries_per_wg<D>() - 1) / queries_per_wg<D>();
   hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.n_wg_q), dim3(kBwdThreads), 0, stream, a, nqb);
   return hipGetLastError();
 }
@@ -615,6 +655,15 @@ hipError_t sum_d(const SumArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+int bwd_queries_per_workgroup(int d) {
+  switch (d) {
+    case 64: return queries_per_wg<64>();
+    case 96: return queries_per_wg<96>();
+    case 128: return queries_per_wg<128>();
+    default: return 0;
+  }
+}
 
 int bwd_keys_per_workgroup(int d) {
   switch (d) {

@@ -317,7 +317,8 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
   const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
-  const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
+  const int qpw = ta::bwd_queries_per_workgroup(d);
+  const int64_t nqb = (T + qpw - 1) / qpw;
   const int kpw = ta::bwd_keys_per_workgroup(d);
   const int64_t nkb = (T + kpw - 1) / kpw;
   const size_t part_row = (size_t)B * T * d * sizeof(float);
@@ -526,9 +527,10 @@ int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out, 
     if (reinterpret_cast<uintptr_t>(p) % 16)
       return fail(TA_ERR_ALIGN, "q, k, v, out, dout, dq, dk and dv must be 16-byte aligned");
   if (reinterpret_cast<uintptr_t>(lse) % 4) return fail(TA_ERR_ALIGN, "lse must be 4-byte aligned");
-  const int kpw = ta::bwd_keys_per_workgroup(d);
-  if ((int64_t)B * H * F * ((T + kpw - 1) / kpw) * ta::kThreads > (int64_t)UINT32_MAX)
-    return fail(TA_ERR_BAD_SHAPE, "the key-side pass would exceed the grid limit");
+  const int kpw = ta::bwd_keys_per_workgroup(d), qpw = ta::bwd_queries_per_workgroup(d);
+  if ((int64_t)B * H * F * ((T + std::min(kpw, qpw) - 1) / std::min(kpw, qpw)) * ta::kThreads >
+      (int64_t)UINT32_MAX)
+    return fail(TA_ERR_BAD_SHAPE, "the gradient passes would exceed the grid limit");
   const size_t bytes = (size_t)B * H * F * T * d * 2;
   const size_t lbytes = (size_t)B * H * F * T * sizeof(float);
   const void* outs[3] = {dq, dk, dv};
