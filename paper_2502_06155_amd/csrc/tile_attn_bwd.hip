@@ -49,26 +49,17 @@ namespace {
 
 constexpr int kBwdWaves = 4;
 constexpr int kBwdThreads = 64 * kBwdWaves;
-// Rows per wave, as 32-row column blocks: query blocks in the dq pass, key blocks
-// in the dk/dv pass. One block per wave keeps every operand, accumulator and score
-// in 256 VGPRs, so two workgroups share a CU and one wave's softmax-gradient
-// arithmetic overlaps the other's matrix instructions; measured at the 93-frame
-// shape this beats two blocks per wave at one workgroup per CU (which halves the
-// LDS fragment reads per MFMA but puts the accumulators in AGPRs and serialises
-// the vector work) by 17% (dq) and 12% (dk/dv). At d = 128 the dk/dv pass needs
-// more than 256 registers and runs one workgroup per CU.
+// Each wave owns one 32-row column block (32 queries in the dq pass, 32 keys in
+// the dk/dv pass). That keeps every operand, accumulator and score in 256 VGPRs,
+// so two workgroups share a CU and one wave's softmax-gradient arithmetic overlaps
+// the other's matrix instructions. Measured at the 93-frame shape this beats 64
+// rows per wave at one workgroup per CU (which halves the LDS fragment reads per
+// MFMA but puts the accumulators in AGPRs, copies the scores out of them and
+// serialises the vector work) by 17% (dq) and 12% (dk/dv). At d = 128 the dk/dv
+// pass needs more than 256 registers and runs one workgroup per CU.
+constexpr int kRowsPerWg = kBwdWaves * 32;
 template <int D>
-constexpr int q_blocks() { return 1; }
-template <int D>
-constexpr int key_blocks() { return 1; }
-template <int D>
-constexpr int dq_occupancy() { return q_blocks<D>() == 2 ? 1 : 2; }
-template <int D>
-constexpr int dkdv_occupancy() { return key_blocks<D>() == 2 || D == 128 ? 1 : 2; }
-template <int D>
-constexpr int queries_per_wg() { return kBwdWaves * 32 * q_blocks<D>(); }
-template <int D>
-constexpr int keys_per_wg() { return kBwdWaves * 32 * key_blocks<D>(); }
+constexpr int dkdv_occupancy() { return D == 128 ? 1 : 2; }
 
 template <int D>
 struct BShape {
@@ -243,6 +234,16 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restric
 }
 
 // ---------------------------------------------------------------------------
+// P = exp2(c s - lse2) clamped to [0, 1] (the clamp folds into the exponential's
+// output modifier). For kept keys the exponent is <= 0 up to rounding, so the clamp
+// changes nothing but rounding; it keeps P finite for the rows and keys past a
+// tile's valid range, whose zero-filled operands then contribute exactly nothing
+// (see the kernels), so no tile needs a mask.
+__device__ __forceinline__ float prob(float s, float c, float lse2) {
+  return __builtin_amdgcn_fmed3f(fast_exp2(__builtin_fmaf(s, c, -lse2)), 0.f, 1.f);
+}
+
+// ---------------------------------------------------------------------------
 // dq pass.
 //
 // dS^T of one 32-key block for one column block, as the B operand of
@@ -254,29 +255,16 @@ __device__ __forceinline__ void dq_scores(const f32x16& s, const f32x16& dp, flo
     f32x8 x;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float p = fast_exp2(__builtin_fmaf(s[8 * c2 + e], c, -lse2));
+      const float p = prob(s[8 * c2 + e], c, lse2);
       x[e] = p * (dp[8 * c2 + e] - dlt);
     }
     ds[c2] = __builtin_convertvector(x, bf16x8);
   }
 }
 
-// Keys of block kb past the tile's valid rows get -inf: P = 0.
-__device__ __forceinline__ void mask_keys(f32x16& s, int kb, int hf, int nvalid) {
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int key = kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-    if (key >= nvalid) s[r] = -INFINITY;
-  }
-}
-
 template <int D>
-__global__ __launch_bounds__(kBwdThreads, dq_occupancy<D>()) void bwd_dq_kernel(const BwdArgs a,
-                                                                                 int nqb) {
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a, int nqb) {
   using Sh = BShape<D>;
-  constexpr int QB = q_blocks<D>();
-  constexpr int kWaveRows = 32 * QB;
-  constexpr int kWgRows = kBwdWaves * kWaveRows;
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
 
@@ -297,27 +285,21 @@ __global__ __launch_bounds__(kBwdThreads, dq_occupancy<D>()) void bwd_dq_kernel(
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hf = lane >> 5;
-  const int qrow0 = qb * kWgRows + wave * kWaveRows + n;
-  const bool wave_active = qb * kWgRows + wave * kWaveRows < T;
+  const int qrow = qb * kRowsPerWg + wave * 32 + n;
+  const bool wave_active = qb * kRowsPerWg + wave * 32 < T;
 
-  bf16x8 qf[QB][Sh::kChunks], gf[QB][Sh::kChunks];
-  float lse2[QB], dlt[QB];
-#pragma unroll
-  for (int qs = 0; qs < QB; ++qs) {
-    const int qrow = qrow0 + 32 * qs;
-    const bool valid = qrow < T;
-    const size_t r = ((size_t)bh * a.F + frame) * T + qrow;
-    load_row_operand<D>(a.q + r * D, valid, a.keep, a.flip, hf, qf[qs]);
-    load_row_operand<D>(a.dout + r * D, valid, ~0u, 0u, hf, gf[qs]);
-    lse2[qs] = valid ? a.lse2[r] : 0.f;
-    dlt[qs] = valid ? a.delta[r] : 0.f;
-  }
+  // This lane's query: Q^T and dO^T B-operand slices, its lse (base 2) and delta.
+  bf16x8 qf[Sh::kChunks], gf[Sh::kChunks];
+  const bool valid = qrow < T;
+  const size_t qr = ((size_t)bh * a.F + frame) * T + qrow;
+  load_row_operand<D>(a.q + qr * D, valid, a.keep, a.flip, hf, qf);
+  load_row_operand<D>(a.dout + qr * D, valid, ~0u, 0u, hf, gf);
+  const float lse2 = valid ? a.lse2[qr] : 0.f;
+  const float dlt = valid ? a.delta[qr] : 0.f;
 
-  f32x16 acc[QB][Sh::kDBlocks];
+  f32x16 acc[Sh::kDBlocks];
 #pragma unroll
-  for (int qs = 0; qs < QB; ++qs)
-#pragma unroll
-    for (int mb = 0; mb < Sh::kDBlocks; ++mb) acc[qs][mb] = f32x16{};
+  for (int mb = 0; mb < Sh::kDBlocks; ++mb) acc[mb] = f32x16{};
 
   const int tpf = (T + kBlockK - 1) / kBlockK;
   const int n_tiles = n_kept * tpf;
@@ -337,40 +319,24 @@ __global__ __launch_bounds__(kBwdThreads, dq_occupancy<D>()) void bwd_dq_kernel(
     wait_tile_loads();
     __syncthreads();
 
-    // One 32-key block of the tile: S^T and dP^T for the wave's column blocks, the
-    // weights' gradient dS^T, then dQ^T += K^T dS^T.
-    auto key_block = [&](const uint16_t* tk, const uint16_t* tv, int kb, int nvalid) {
-      f32x16 s[QB], dp[QB];
-#pragma unroll
-      for (int qs = 0; qs < QB; ++qs) {
-        s[qs] = f32x16{};
-        dp[qs] = f32x16{};
-      }
+    // S^T and dP^T of 32-key block kb (raw logits; keys past the tile's valid rows
+    // read zero rows).
+    auto scores = [&](const uint16_t* tk, const uint16_t* tv, int kb, f32x16& sc, f32x16& dp) {
+      sc = f32x16{};
+      dp = f32x16{};
 #pragma unroll
       for (int cc = 0; cc < Sh::kChunks; ++cc) {
-        const bf16x8 kx = row_frag<D>(tk, ra, kb, cc);
-        const bf16x8 vx = row_frag<D>(tv, ra, kb, cc);
-#pragma unroll
-        for (int qs = 0; qs < QB; ++qs) {
-          s[qs] = mfma32(kx, qf[qs][cc], s[qs]);
-          dp[qs] = mfma32(vx, gf[qs][cc], dp[qs]);
-        }
+        sc = mfma32(row_frag<D>(tk, ra, kb, cc), qf[cc], sc);
+        dp = mfma32(row_frag<D>(tv, ra, kb, cc), gf[cc], dp);
       }
-      if (nvalid < kBlockK) {
-#pragma unroll
-        for (int qs = 0; qs < QB; ++qs) mask_keys(s[qs], kb, hf, nvalid);
-      }
-      bf16x8 ds[QB][2];
-#pragma unroll
-      for (int qs = 0; qs < QB; ++qs) dq_scores(s[qs], dp[qs], a.c, lse2[qs], dlt[qs], ds[qs]);
+    };
+    // dQ^T += K^T dS^T over block kb.
+    auto accumulate = [&](const uint16_t* tk, int kb, const bf16x8 (&ds)[2]) {
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-        for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
-          const bf16x8 kt = tr_frag<D>(tk, ta, mb, 2 * kb + c2);
-#pragma unroll
-          for (int qs = 0; qs < QB; ++qs) acc[qs][mb] = mfma32(kt, ds[qs][c2], acc[qs][mb]);
-        }
+        for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+          acc[mb] = mfma32(tr_frag<D>(tk, ta, mb, 2 * kb + c2), ds[c2], acc[mb]);
     };
 
     for (int t = 0; t < n_tiles; ++t) {
@@ -379,16 +345,22 @@ __global__ __launch_bounds__(kBwdThreads, dq_occupancy<D>()) void bwd_dq_kernel(
         ld.load(Kh, nxt.key0(), nxt.nvalid(), sK[buf ^ 1], wave);
         ld.load(Vh, nxt.key0(), nxt.nvalid(), sV[buf ^ 1], wave);
       }
-      const int nvalid = cur.nvalid();
       if (wave_active) {
-        if constexpr (QB == 2) {
-          // Not unrolled: the two blocks' fragments would not fit the registers together.
-#pragma unroll 1
-          for (int kb = 0; kb < 2; ++kb) key_block(sK[buf], sV[buf], kb, nvalid);
-        } else {
-          key_block(sK[buf], sV[buf], 0, nvalid);
-          key_block(sK[buf], sV[buf], 1, nvalid);
-        }
+        // Block 1's S/dP run on the matrix cores while block 0's dS forms on the
+        // vector ALUs, then block 0's dQ update while block 1's dS forms. The
+        // scheduling fences keep each phase's fragments and scores from being
+        // hoisted into the previous one (5% faster than leaving the order free).
+        f32x16 s0, dp0, s1, dp1;
+        bf16x8 ds0[2], ds1[2];
+        scores(sK[buf], sV[buf], 0, s0, dp0);
+        __builtin_amdgcn_sched_barrier(0);
+        scores(sK[buf], sV[buf], 1, s1, dp1);
+        dq_scores(s0, dp0, a.c, lse2, dlt, ds0);
+        __builtin_amdgcn_sched_barrier(0);
+        accumulate(sK[buf], 0, ds0);
+        dq_scores(s1, dp1, a.c, lse2, dlt, ds1);
+        __builtin_amdgcn_sched_barrier(0);
+        accumulate(sK[buf], 1, ds1);
       }
       cur = nxt;
       nxt.advance(n_kept);
@@ -397,15 +369,12 @@ __global__ __launch_bounds__(kBwdThreads, dq_occupancy<D>()) void bwd_dq_kernel(
     }
   }
 
-#pragma unroll
-  for (int qs = 0; qs < QB; ++qs) {
-    const int qrow = qrow0 + 32 * qs;
-    if (qrow >= T) continue;
+  if (qrow < T) {
     if (slot < 0) {
-      store_row_bf16<D>(a.dq + (((size_t)bh * a.F + frame) * T + qrow) * D, acc[qs], a.scale, hf);
+      store_row_bf16<D>(a.dq + qr * D, acc, a.scale, hf);
     } else {
       const size_t prow = ((size_t)slot * a.B + b) * T + qrow;
-      store_row_f32<D>(a.ws_dq + prow * D, acc[qs], a.scale, hf);
+      store_row_f32<D>(a.ws_dq + prow * D, acc, a.scale, hf);
     }
   }
 }
@@ -416,8 +385,6 @@ template <int D>
 __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_kernel(const BwdArgs a,
                                                                                      int nkb) {
   using Sh = BShape<D>;
-  constexpr int KB = key_blocks<D>();
-  constexpr int kWgKeys = keys_per_wg<D>();
   __shared__ __attribute__((aligned(1024))) uint16_t sQ[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sG[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(256))) float sL[2][kBlockK];
@@ -442,29 +409,22 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hf = lane >> 5;
-  const int krow0 = kblk * kWgKeys + wave * 32 * KB + n;
-  const bool wave_active = kblk * kWgKeys + wave * 32 * KB < T;
+  const int krow = kblk * kRowsPerWg + wave * 32 + n;
+  const bool wave_active = kblk * kRowsPerWg + wave * 32 < T;
 
-  // This lane's keys (one per 32-key block) as B operands of S = Q K^T and
-  // dP = dO V^T.
-  bf16x8 kf[KB][Sh::kChunks], vf[KB][Sh::kChunks];
+  // This lane's key as B operand of S = Q K^T and dP = dO V^T.
+  bf16x8 kf[Sh::kChunks], vf[Sh::kChunks];
+  const bool valid = krow < T;
+  const size_t kr = ((size_t)bh * a.F + frame) * T + krow;
+  load_row_operand<D>(a.k + kr * D, valid, a.keep, a.flip, hf, kf);
+  load_row_operand<D>(a.v + kr * D, valid, ~0u, 0u, hf, vf);
+
+  f32x16 dk[Sh::kDBlocks], dv[Sh::kDBlocks];
 #pragma unroll
-  for (int kb = 0; kb < KB; ++kb) {
-    const int krow = krow0 + 32 * kb;
-    const bool valid = krow < T;
-    const size_t r = ((size_t)bh * a.F + frame) * T + krow;
-    load_row_operand<D>(a.k + r * D, valid, a.keep, a.flip, hf, kf[kb]);
-    load_row_operand<D>(a.v + r * D, valid, ~0u, 0u, hf, vf[kb]);
+  for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
+    dk[mb] = f32x16{};
+    dv[mb] = f32x16{};
   }
-
-  f32x16 dk[KB][Sh::kDBlocks], dv[KB][Sh::kDBlocks];
-#pragma unroll
-  for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-    for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
-      dk[kb][mb] = f32x16{};
-      dv[kb][mb] = f32x16{};
-    }
 
   const int tpf = (T + kBlockK - 1) / kBlockK;
   const int n_tiles = n_keep * tpf;
@@ -475,6 +435,8 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
     ra.init(n, hf);
     TrAddr<D> ta;
     ta.init(lane);
+    // Q, dO, lse2 and delta of one 64-query tile; rows past the valid range read
+    // as zeros, so they add exactly nothing below (zero Q and dO rows, P <= 1).
     auto load_tile = [&](const TileCursor& tc, int bi) {
       const size_t row0 = tc.key0();
       const int nv = tc.nvalid();
@@ -495,77 +457,65 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
     wait_tile_loads();
     __syncthreads();
 
+    // S and dP of 32-query half qc of the tile.
+    auto scores = [&](int buf, int qc, f32x16& sc, f32x16& dp) {
+      sc = f32x16{};
+      dp = f32x16{};
+#pragma unroll
+      for (int cc = 0; cc < Sh::kChunks; ++cc) {
+        sc = mfma32(row_frag<D>(sQ[buf], ra, qc, cc), kf[cc], sc);
+        dp = mfma32(row_frag<D>(sG[buf], ra, qc, cc), vf[cc], dp);
+      }
+    };
+    // P and dS of half qc as B operands (entry 8 c2 + 4u + j holds query row
+    // 32 qc + 16 c2 + 8u + 4h + j).
+    auto grads = [&](int buf, int qc, const f32x16& sc, const f32x16& dp, bf16x8 (&pb)[2],
+                     bf16x8 (&db)[2]) {
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        f32x8 p8, d8;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sL[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int e = 8 * c2 + 4 * u + j;
+            const float p = prob(sc[e], a.c, l4[j]);
+            p8[4 * u + j] = p;
+            d8[4 * u + j] = p * (dp[e] - d4[j]);
+          }
+        }
+        pb[c2] = __builtin_convertvector(p8, bf16x8);
+        db[c2] = __builtin_convertvector(d8, bf16x8);
+      }
+    };
+    // dV^T += dO^T P and dK^T += Q^T dS over half qc.
+    auto accumulate = [&](int buf, int qc, const bf16x8 (&pb)[2], const bf16x8 (&db)[2]) {
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+        for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
+          dv[mb] = mfma32(tr_frag<D>(sG[buf], ta, mb, 2 * qc + c2), pb[c2], dv[mb]);
+          dk[mb] = mfma32(tr_frag<D>(sQ[buf], ta, mb, 2 * qc + c2), db[c2], dk[mb]);
+        }
+    };
+
     for (int t = 0; t < n_tiles; ++t) {
       const int buf = t & 1;
       if (t + 1 < n_tiles) load_tile(nxt, buf ^ 1);
-      const int nvalid = cur.nvalid();
       if (wave_active) {
-        // One 32-query half of the tile at a time (not unrolled: the halves would
-        // otherwise be interleaved past the register budget).
-#pragma unroll 1
-        for (int qc = 0; qc < 2; ++qc) {
-          f32x16 s[KB], dp[KB];
-#pragma unroll
-          for (int kb = 0; kb < KB; ++kb) {
-            s[kb] = f32x16{};
-            dp[kb] = f32x16{};
-          }
-#pragma unroll
-          for (int cc = 0; cc < Sh::kChunks; ++cc) {
-            const bf16x8 qx = row_frag<D>(sQ[buf], ra, qc, cc);
-            const bf16x8 gx = row_frag<D>(sG[buf], ra, qc, cc);
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) {
-              s[kb] = mfma32(qx, kf[kb][cc], s[kb]);
-              dp[kb] = mfma32(gx, vf[kb][cc], dp[kb]);
-            }
-          }
-          if (nvalid < kBlockK) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int qr = 32 * qc + 8 * (e >> 2) + 4 * hf + (e & 3);
-              if (qr >= nvalid) {
-#pragma unroll
-                for (int kb = 0; kb < KB; ++kb) s[kb][e] = -INFINITY;
-              }
-            }
-          }
-          // Entry 8 c2 + 4 u + j holds query row 32 qc + 16 c2 + 8u + 4h + j.
-          bf16x8 pb[KB][2], db[KB][2];
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2) {
-            f32x4 l4[2], d4[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              l4[u] = *reinterpret_cast<const f32x4*>(&sL[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
-              d4[u] = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
-            }
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) {
-              f32x8 p8, d8;
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                const float p = fast_exp2(__builtin_fmaf(s[kb][8 * c2 + e], a.c, -l4[e >> 2][e & 3]));
-                p8[e] = p;
-                d8[e] = p * (dp[kb][8 * c2 + e] - d4[e >> 2][e & 3]);
-              }
-              pb[kb][c2] = __builtin_convertvector(p8, bf16x8);
-              db[kb][c2] = __builtin_convertvector(d8, bf16x8);
-            }
-          }
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-            for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
-              const bf16x8 gt = tr_frag<D>(sG[buf], ta, mb, 2 * qc + c2);
-              const bf16x8 qt = tr_frag<D>(sQ[buf], ta, mb, 2 * qc + c2);
-#pragma unroll
-              for (int kb = 0; kb < KB; ++kb) {
-                dv[kb][mb] = mfma32(gt, pb[kb][c2], dv[kb][mb]);
-                dk[kb][mb] = mfma32(qt, db[kb][c2], dk[kb][mb]);
-              }
-            }
-        }
+        // Program order puts half 1's S/dP ahead of half 0's P and dS and half 0's
+        // dV/dK update ahead of half 1's P and dS; the compiler interleaves them
+        // (fencing the phases, as in the dq pass, measured 4% slower here).
+        f32x16 s0, dp0, s1, dp1;
+        bf16x8 pb0[2], db0[2], pb1[2], db1[2];
+        scores(buf, 0, s0, dp0);
+        scores(buf, 1, s1, dp1);
+        grads(buf, 0, s0, dp0, pb0, db0);
+        accumulate(buf, 0, pb0, db0);
+        grads(buf, 1, s1, dp1, pb1, db1);
+        accumulate(buf, 1, pb1, db1);
       }
       cur = nxt;
       nxt.advance(n_keep);
@@ -575,18 +525,14 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   }
 
   // dK uses the unflipped q of the LDS tiles, so scale (with its sign) applies.
-#pragma unroll
-  for (int kb = 0; kb < KB; ++kb) {
-    const int krow = krow0 + 32 * kb;
-    if (krow >= T) continue;
+  if (krow < T) {
     if (slot < 0) {
-      const size_t r = ((size_t)bh * a.F + frame) * T + krow;
-      store_row_bf16<D>(a.dk + r * D, dk[kb], a.scale, hf);
-      store_row_bf16<D>(a.dv + r * D, dv[kb], 1.f, hf);
+      store_row_bf16<D>(a.dk + kr * D, dk, a.scale, hf);
+      store_row_bf16<D>(a.dv + kr * D, dv, 1.f, hf);
     } else {
       const size_t prow = ((size_t)slot * a.B + b) * T + krow;
-      store_row_f32<D>(a.ws_dk + prow * D, dk[kb], a.scale, hf);
-      store_row_f32<D>(a.ws_dv + prow * D, dv[kb], 1.f, hf);
+      store_row_f32<D>(a.ws_dk + prow * D, dk, a.scale, hf);
+      store_row_f32<D>(a.ws_dv + prow * D, dv, 1.f, hf);
     }
   }
 }
@@ -633,14 +579,14 @@ hipError_t prep_d(const PrepArgs& a, hipStream_t stream) {
 
 template <int D>
 hipError_t dq_d(const BwdArgs& a, hipStream_t stream) {
-  const int nqb = (a.T + queries_per_wg<D>() - 1) / queries_per_wg<D>();
+  const int nqb = (a.T + kRowsPerWg - 1) / kRowsPerWg;
   hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.n_wg_q), dim3(kBwdThreads), 0, stream, a, nqb);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t dkdv_d(const BwdArgs& a, hipStream_t stream) {
-  const int nkb = (a.T + keys_per_wg<D>() - 1) / keys_per_wg<D>();
+  const int nkb = (a.T + kRowsPerWg - 1) / kRowsPerWg;
   hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream, a, nkb);
   return hipGetLastError();
 }
@@ -656,23 +602,9 @@ hipError_t sum_d(const SumArgs& a, hipStream_t stream) {
 
 }  // namespace
 
-int bwd_queries_per_workgroup(int d) {
-  switch (d) {
-    case 64: return queries_per_wg<64>();
-    case 96: return queries_per_wg<96>();
-    case 128: return queries_per_wg<128>();
-    default: return 0;
-  }
-}
+int bwd_queries_per_workgroup(int) { return kRowsPerWg; }
 
-int bwd_keys_per_workgroup(int d) {
-  switch (d) {
-    case 64: return keys_per_wg<64>();
-    case 96: return keys_per_wg<96>();
-    case 128: return keys_per_wg<128>();
-    default: return 0;
-  }
-}
+int bwd_keys_per_workgroup(int) { return kRowsPerWg; }
 
 #define TA_DISPATCH_D(fn, a, stream)          \
   switch ((a).d) {                            \

@@ -242,21 +242,6 @@ __device__ __forceinline__ float block_weights(const f32x16& s, float c, float m
   return ls;
 }
 
-// Scheduling hint for a region holding N_MFMA matrix instructions (with their LDS
-// fragment reads) and about N_VALU vector instructions that do not depend on
-// them: each MFMA is followed by a share of the VALU work, so the vector ALUs
-// issue while the matrix core runs.
-template <int N_MFMA, int N_VALU>
-__device__ __forceinline__ void interleave_mfma_valu() {
-  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
-#pragma unroll
-  for (int i = 0; i < N_MFMA; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x002, (N_VALU + N_MFMA - 1) / N_MFMA, 0);  // VALU
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                        // DS read
-  }
-}
-
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,

@@ -121,5 +121,20 @@ __device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
       (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)p));
 }
 
+// Scheduling hint for a region holding N_MFMA matrix instructions (with their LDS
+// fragment reads) and about N_VALU vector instructions that do not depend on
+// them: each MFMA is followed by a share of the VALU work, so the vector ALUs
+// issue while the matrix core runs.
+template <int N_MFMA, int N_VALU>
+__device__ __forceinline__ void interleave_mfma_valu() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
+#pragma unroll
+  for (int i = 0; i < N_MFMA; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, (N_VALU + N_MFMA - 1) / N_MFMA, 0);  // VALU
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                        // DS read
+  }
+}
+
 }  // namespace
 }  // namespace ta
