@@ -8,9 +8,11 @@ computes, written from the paper (Efficient-vDiT, arXiv 2502.06155):
 * ``oracle.attention``: softmax attention restricted to the key frames a query
   frame's mask row keeps (Sec. 3.1, Sec. 3.3, App. B), and its log-sum-exp.
 * ``oracle.backward``: the gradients of that attention with respect to q, k, v.
+* ``oracle.mmdit``: the MM-DiT form, a dense text prefix before the tile-sparse video
+  (Sec. 4.3, App. E).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package. The product path (the HIP library and
 its Python binding) never imports it, and it imports nothing from the product.
 """
-from . import attention, backward, masks  # noqa: F401
+from . import attention, backward, masks, mmdit  # noqa: F401

@@ -320,3 +320,102 @@ def pin_bwd_uniform_weights(bwd):
 
 
 BWD_PINS = [pin_bwd_matches_autograd, pin_bwd_bruteforce, pin_bwd_uniform_weights]
+
+
+# ---- pins of the MM-DiT form: fn(q, k, v, mask, T, P, scale) -> out --------------------
+
+def _mmdit_token_mask(mask_h, F, T, P):
+    """Boolean [S, S] token mask: text rows and text columns all kept, video-video part
+    from the frame mask."""
+    S = P + F * T
+    tok = np.zeros((S, S), dtype=bool)
+    tok[:P, :] = True
+    tok[:, :P] = True
+    fr = np.arange(F * T) // T
+    tok[P:, P:] = np.asarray(mask_h, dtype=bool)[fr][:, fr]
+    return tok
+
+
+def pin_mmdit_matches_sdpa_token_mask(fn):
+    rng = np.random.default_rng(30)
+    for (B, H, F, T, P, d) in [(1, 2, 3, 4, 5, 8), (2, 3, 4, 3, 1, 6), (1, 2, 5, 2, 7, 4)]:
+        q, k, v = (_rand(rng, B, H, P + F * T, d) for _ in range(3))
+        masks = (rng.random((H, F, F)) < 0.4).astype(np.uint8)
+        masks[0, 1, :] = 0  # a video frame keeping no video frame still sees the text
+        got = fn(q, k, v, masks, T, P, 0.7)
+        for h in range(H):
+            tok = torch.from_numpy(_mmdit_token_mask(masks[h], F, T, P))
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(q[:, h]), torch.from_numpy(k[:, h]), torch.from_numpy(v[:, h]),
+                attn_mask=tok, scale=0.7).numpy()
+            assert np.max(np.abs(got[:, h] - ref)) < TOL
+
+
+def pin_mmdit_dense_is_plain_attention_over_all_tokens(fn):
+    rng = np.random.default_rng(31)
+    B, H, F, T, P, d = 2, 2, 3, 5, 4, 8
+    q, k, v = (_rand(rng, B, H, P + F * T, d) for _ in range(3))
+    got = fn(q, k, v, np.ones((F, F), np.uint8), T, P, 0.3)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v), scale=0.3).numpy()
+    assert np.max(np.abs(got - ref)) < TOL
+
+
+def pin_mmdit_bruteforce(fn):
+    """Token by token in pure Python, from the stated rule."""
+    rng = np.random.default_rng(32)
+    F, T, P, d, scale = 3, 2, 2, 3, 0.9
+    mask = np.array([[1, 0, 0], [0, 0, 0], [1, 1, 0]], np.uint8)
+    q, k, v = (_rand(rng, 1, 1, P + F * T, d, 0.8) for _ in range(3))
+    got = fn(q, k, v, mask, T, P, scale)
+    S = P + F * T
+    for s in range(S):
+        if s < P:
+            keys = list(range(S))
+        else:
+            i = (s - P) // T
+            keys = [t for t in range(S) if t < P or mask[i][(t - P) // T]]
+        w = [math.exp(scale * sum(q[0, 0, s, c] * k[0, 0, t, c] for c in range(d))) for t in keys]
+        z = sum(w)
+        for c in range(d):
+            ref = sum(wi * v[0, 0, t, c] for wi, t in zip(w, keys)) / z
+            assert abs(got[0, 0, s, c] - ref) < TOL
+
+
+def pin_mmdit_text_queries_ignore_the_mask(fn):
+    """Invariant: text rows attend to everything, so no mask changes them; and with
+    identical video frames a video row's output depends only on how many frames it
+    keeps (here: frame 1 keeps one frame, frame 2 keeps one other frame)."""
+    rng = np.random.default_rng(33)
+    F, T, P, d = 3, 4, 3, 5
+    q, k, v = (_rand(rng, 1, 1, P + F * T, d) for _ in range(3))
+    a = fn(q, k, v, np.eye(F, dtype=np.uint8), T, P, 0.5)
+    b = fn(q, k, v, np.ones((F, F), np.uint8), T, P, 0.5)
+    assert np.max(np.abs(a[0, 0, :P] - b[0, 0, :P])) < TOL
+    kk, vv = k.copy(), v.copy()
+    for j in range(1, F):
+        kk[0, 0, P + j * T:P + (j + 1) * T] = kk[0, 0, P:P + T]
+        vv[0, 0, P + j * T:P + (j + 1) * T] = vv[0, 0, P:P + T]
+    m = np.array([[1, 0, 0], [0, 0, 1], [1, 0, 0]], np.uint8)
+    got = fn(q, kk, vv, m, T, P, 0.5)
+    m2 = np.array([[1, 0, 0], [1, 0, 0], [0, 1, 0]], np.uint8)
+    got2 = fn(q, kk, vv, m2, T, P, 0.5)
+    assert np.max(np.abs(got[0, 0, P + T:] - got2[0, 0, P + T:])) < TOL
+
+
+MMDIT_PINS = [pin_mmdit_matches_sdpa_token_mask, pin_mmdit_dense_is_plain_attention_over_all_tokens,
+              pin_mmdit_bruteforce, pin_mmdit_text_queries_ignore_the_mask]
+
+
+def pin_mmdit_lse(lse_fn):
+    """The MM-DiT log-sum-exp against torch.logsumexp over the token mask."""
+    rng = np.random.default_rng(34)
+    B, H, F, T, P, d = 1, 2, 4, 3, 5, 6
+    q, k = (_rand(rng, B, H, P + F * T, d) for _ in range(2))
+    masks = (rng.random((H, F, F)) < 0.5).astype(np.uint8)
+    got = lse_fn(q, k, masks, T, P, 0.8)
+    for h in range(H):
+        tok = torch.from_numpy(_mmdit_token_mask(masks[h], F, T, P))
+        logits = 0.8 * torch.from_numpy(q[:, h]) @ torch.from_numpy(k[:, h]).transpose(-1, -2)
+        ref = torch.logsumexp(logits.masked_fill(~tok, float("-inf")), dim=-1).numpy()
+        assert np.max(np.abs(got[:, h] - ref)) < TOL
