@@ -102,6 +102,28 @@ int tile_attn_fwd_heads(const void* q, const void* k, const void* v, void* out,
                         float* lse, void* stream);
 
 /*
+ * The MM-DiT form (Sec. 4.3 and App. E: CogVideoX concatenates text tokens with
+ * the video tokens and the sparse mask covers only the video-video part). Each
+ * (batch, head) sequence holds P text tokens first, then the F * T video tokens
+ * frame-major: S = P + F * T. A text query attends to all S tokens; a query of
+ * video frame i attends to the P text tokens and to the tokens of the video frames
+ * its mask row keeps.
+ *
+ * q, k, v, out: DEVICE bf16 [B, H, P + F*T, d], 16-byte aligned. P >= 0 (P = 0
+ *   is tile_attn_fwd_heads). tile_masks, n_masks: F x F video masks as for
+ *   tile_attn_fwd_heads. lse: as for tile_attn_fwd_heads over the S rows, or NULL.
+ *   The text queries keep every segment, so their work is split into pieces like
+ *   any heavy query frame (tile_attn_plan of the (F+1) x (F+1) mask whose last row
+ *   and column, the text, are all ones).
+ * Errors: those of tile_attn_fwd_heads; TA_ERR_BAD_SHAPE also for P < 0 or
+ *   P + F*T > 2^31 - 1.
+ */
+int tile_attn_fwd_mmdit(const void* q, const void* k, const void* v, void* out,
+                        int B, int H, int F, int T, int P, int d,
+                        const uint8_t* tile_masks, int n_masks, float scale,
+                        float* lse, void* stream);
+
+/*
  * Gradients of tile-sparse attention (the op the sparse student of Sec. 3.4 is
  * trained through). With P[s,t] = exp(scale * <q[s], k[t]> - lse[s]) over the kept
  * pairs, dP[s,t] = <dout[s], v[t]>, delta[s] = <dout[s], out[s]> and

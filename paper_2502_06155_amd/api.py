@@ -74,6 +74,19 @@ def tile_attn_fwd_heads(q, k, v, out, B: int, H: int, F: int, T: int, d: int, ti
                                    _stream(stream)), "tile_attn_fwd_heads")
 
 
+def tile_attn_fwd_mmdit(q, k, v, out, B: int, H: int, F: int, T: int, P: int, d: int,
+                        tile_masks, scale: float, lse=None, stream=None) -> None:
+    """tile_attn_fwd_mmdit of the C ABI: P text tokens before the F*T video tokens
+    ([B, H, P + F*T, d]); tile_masks (F x F or H x F x F) cover the video part only."""
+    m = np.ascontiguousarray(np.asarray(tile_masks), dtype=np.uint8)
+    if m.size % (F * F):
+        raise ValueError("tile_masks must hold n_masks * F * F entries")
+    n_masks = m.size // (F * F)
+    _check(lib.tile_attn_fwd_mmdit(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, F, T, P, d,
+                                   m.ctypes.data, n_masks, float(scale), _ptr(lse),
+                                   _stream(stream)), "tile_attn_fwd_mmdit")
+
+
 def tile_attn_bwd(q, k, v, out, dout, lse, dq, dk, dv, B: int, H: int, F: int, T: int,
                   d: int, tile_masks, scale: float, stream=None) -> None:
     """tile_attn_bwd of the C ABI: gradients dq, dk, dv (bf16 [B, H, F*T, d]) from the

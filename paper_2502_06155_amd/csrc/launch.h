@@ -15,6 +15,9 @@ struct FwdArgs {
   const uint16_t* v;
   uint16_t* out;
   int B, H, F, T, d;
+  // Text tokens before the F*T video tokens (MM-DiT form), or 0. With P > 0 the
+  // work items address F + 1 segments: frames 0..F-1 at P + j*T, the text as F.
+  int P;
   // Work items, 5 int32 each, in dispatch order: {head, query frame, first kept
   // entry in cols, number of kept entries, partial slot or -1}. Every batch entry
   // runs every item. A query frame with many kept frames is split into several
@@ -23,13 +26,13 @@ struct FwdArgs {
   const int32_t* items;
   const int32_t* cols;  // kept key frames, row after row, head after head
   int n_items;          // items over all heads
-  float* ws_o;          // partial O/l, fp32 [n_slots][B][T][d] (null if no slots)
-  float* ws_lse;        // partial base-2 log-sum-exp, fp32 [n_slots][B][T]
-  float* lse;           // natural-log log-sum-exp out, fp32 [B][H][F*T], or null
+  float* ws_o;          // partial O/l, fp32 [n_slots][B][max(T,P)][d] (null if no slots)
+  float* ws_lse;        // partial base-2 log-sum-exp, fp32 [n_slots][B][max(T,P)]
+  float* lse;           // natural-log log-sum-exp out, fp32 [B][H][P+F*T], or null
   float c;              // > 0: |scale| * log2(e), logits in base-2 units
   uint32_t qflip;       // 0x80008000 flips the sign of q (negative scale), else 0
   uint32_t qmask;       // 0 zeroes q (scale 0: exactly uniform weights), else ~0
-  uint32_t n_wg;        // B * n_items * ceil(T / kBlockQ)
+  uint32_t n_wg;        // B * n_items * ceil(max(T, P) / kBlockQ)
 };
 
 // Combines the partial results of split query frames: heavy holds 4 int32 per split
@@ -40,6 +43,7 @@ struct MergeArgs {
   const int32_t* heavy;
   int n_heavy;
   int B, H, F, T, d;
+  int P;       // text tokens before the video (0: none)
   uint16_t* out;
   float* lse;  // natural-log log-sum-exp out or null
 };

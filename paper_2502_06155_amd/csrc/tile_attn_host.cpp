@@ -130,22 +130,23 @@ bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 int check_args(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
-               int T, int d, float scale) {
+               int T, int d, float scale, int P = 0) {
   if (!q || !k || !v || !out) return fail(TA_ERR_NULL_PTR, "q, k, v and out must be non-NULL");
   if (B < 1 || H < 1 || F < 1 || T < 1)
     return fail(TA_ERR_BAD_SHAPE, "B, H, F and T must be >= 1");
+  if (P < 0) return fail(TA_ERR_BAD_SHAPE, "the text prefix length must be >= 0");
   if (F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F exceeds TA_MAX_FRAMES");
-  if ((int64_t)F * T > INT32_MAX) return fail(TA_ERR_BAD_SHAPE, "F * T exceeds 2^31 - 1");
+  if ((int64_t)F * T + P > INT32_MAX) return fail(TA_ERR_BAD_SHAPE, "P + F * T exceeds 2^31 - 1");
   if (d != 64 && d != 96 && d != 128) return fail(TA_ERR_HEAD_DIM, "d must be 64, 96 or 128");
-  const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
-  const int64_t n_wg = (int64_t)B * H * F * nqb;
+  const int64_t nqb = (std::max(T, P) + ta::kBlockQ - 1) / ta::kBlockQ;
+  const int64_t n_wg = (int64_t)B * H * (F + (P > 0)) * nqb;
   if (n_wg * ta::kThreads > (int64_t)UINT32_MAX)
     return fail(TA_ERR_BAD_SHAPE, "B * H * F * ceil(T / 256) workgroups exceed the grid limit");
   if (!std::isfinite(scale)) return fail(TA_ERR_BAD_SCALE, "scale must be finite");
   for (const void* p : {q, k, v, (const void*)out})
     if (reinterpret_cast<uintptr_t>(p) % 16)
       return fail(TA_ERR_ALIGN, "q, k, v and out must be 16-byte aligned");
-  const size_t bytes = (size_t)B * H * F * T * d * 2;
+  const size_t bytes = (size_t)B * H * ((size_t)F * T + P) * d * 2;
   for (const void* p : {q, k, v})
     if (ranges_overlap(out, bytes, p, bytes)) return fail(TA_ERR_OVERLAP, "out overlaps an input");
   return TA_OK;
@@ -235,23 +236,38 @@ int workspace_for(int dev, void* stream, size_t bytes, void** out) {
 }
 
 int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F, int T,
-            int d, const uint8_t* masks, int n_masks, float scale, float* lse, void* stream) {
+            int d, const uint8_t* masks, int n_masks, float scale, float* lse, void* stream,
+            int P = 0) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
-  const int64_t nqb = (T + ta::kBlockQ - 1) / ta::kBlockQ;
+  const int L = std::max(T, P);  // longest segment: rows per query-block grid column
+  const int64_t nqb = (L + ta::kBlockQ - 1) / ta::kBlockQ;
+  // With a text prefix, plan F + 1 segments: video row i keeps its mask row plus the
+  // text (segment F); the text row keeps everything.
+  std::vector<uint8_t> aug;
+  int n_seg = F;
+  if (P > 0) {
+    n_seg = F + 1;
+    aug.assign((size_t)n_masks * n_seg * n_seg, 1);
+    for (int m = 0; m < n_masks; ++m)
+      for (int i = 0; i < F; ++i)
+        for (int j = 0; j < F; ++j)
+          aug[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * F + i) * F + j] ? 1 : 0;
+    masks = aug.data();
+  }
   const DeviceWorkList* wl = nullptr;
-  int st = work_list_for(masks, n_masks, H, F, true, dev, &wl);
+  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &wl);
   if (st != TA_OK) return st;
   const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
-  if ((size_t)wl->n_slots * B * T * (d + 1) * sizeof(float) > kMaxWorkspaceBytes ||
+  if ((size_t)wl->n_slots * B * L * (d + 1) * sizeof(float) > kMaxWorkspaceBytes ||
       (int64_t)B * wl->n_items * nqb > max_wg) {
-    st = work_list_for(masks, n_masks, H, F, false, dev, &wl);  // the same frames, not split
+    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &wl);  // the same rows, not split
     if (st != TA_OK) return st;
   }
   void* ws = nullptr;
   if (wl->n_slots > 0) {
-    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * T * (d + 1) * sizeof(float), &ws);
+    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * L * (d + 1) * sizeof(float), &ws);
     if (st != TA_OK) return st;
   }
   ta::FwdArgs a;
@@ -264,11 +280,12 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   a.F = F;
   a.T = T;
   a.d = d;
+  a.P = P;
   a.items = wl->items;
   a.cols = wl->cols;
   a.n_items = wl->n_items;
   a.ws_o = static_cast<float*>(ws);
-  a.ws_lse = ws ? static_cast<float*>(ws) + (size_t)wl->n_slots * B * T * d : nullptr;
+  a.ws_lse = ws ? static_cast<float*>(ws) + (size_t)wl->n_slots * B * L * d : nullptr;
   a.lse = lse;
   // Logits are formed from |scale| (a negative scale flips the sign of q, which
   // is exact in bf16). scale == 0 zeroes q instead, so every logit is exactly 0
@@ -296,6 +313,7 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
     m.F = F;
     m.T = T;
     m.d = d;
+    m.P = P;
     m.out = a.out;
     m.lse = lse;
     e = ta::launch_merge_partials(m, static_cast<hipStream_t>(stream));
@@ -504,6 +522,24 @@ int tile_attn_fwd_heads(const void* q, const void* k, const void* v, void* out, 
       if (ranges_overlap(lse, lbytes, p, bytes)) return fail(TA_ERR_OVERLAP, "lse overlaps a tensor");
   }
   return run_fwd(q, k, v, out, B, H, F, T, d, tile_masks, n_masks, scale, lse, stream);
+}
+
+int tile_attn_fwd_mmdit(const void* q, const void* k, const void* v, void* out, int B, int H,
+                        int F, int T, int P, int d, const uint8_t* tile_masks, int n_masks,
+                        float scale, float* lse, void* stream) {
+  int st = check_args(q, k, v, out, B, H, F, T, d, scale, P);
+  if (st != TA_OK) return st;
+  if (!tile_masks) return fail(TA_ERR_NULL_PTR, "tile_masks must be non-NULL");
+  if (n_masks != 1 && n_masks != H) return fail(TA_ERR_BAD_MASK, "n_masks must be 1 or H");
+  if (F + (P > 0) > TA_MAX_FRAMES + 1) return fail(TA_ERR_BAD_SHAPE, "F exceeds TA_MAX_FRAMES");
+  if (lse) {
+    if (reinterpret_cast<uintptr_t>(lse) % 4) return fail(TA_ERR_ALIGN, "lse must be 4-byte aligned");
+    const size_t rows = (size_t)B * H * ((size_t)F * T + P);
+    for (const void* p : {q, k, v, (const void*)out})
+      if (ranges_overlap(lse, rows * sizeof(float), p, rows * d * 2))
+        return fail(TA_ERR_OVERLAP, "lse overlaps a tensor");
+  }
+  return run_fwd(q, k, v, out, B, H, F, T, d, tile_masks, n_masks, scale, lse, stream, P);
 }
 
 int dense_attn_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,

@@ -49,6 +49,8 @@
 #include <hip/hip_runtime.h>
 
 #include <float.h>
+
+#include <algorithm>
 #include <stdint.h>
 
 #include "launch.h"
@@ -242,13 +244,59 @@ __device__ __forceinline__ float block_weights(const f32x16& s, float c, float m
   return ls;
 }
 
-template <int D>
+// Token layout of one (batch, head). Without a prefix: F frames of T tokens,
+// segment j = frame j at j*T. With a prefix (the MM-DiT form): P text tokens first,
+// then the frames, so segment j < F starts at P + j*T and segment F is the text,
+// P tokens at 0.
+template <bool PREFIX>
+struct Layout {
+  int F, T, P;
+  __device__ __forceinline__ int start(int j) const {
+    if constexpr (PREFIX) return j < F ? P + j * T : 0;
+    else return j * T;
+  }
+  __device__ __forceinline__ int len(int j) const {
+    if constexpr (PREFIX) return j < F ? T : P;
+    else return T;
+  }
+};
+
+// Walks the 64-token tiles of a list of segments (frames, and the text segment with
+// a prefix) in order; all state is wave-uniform. Without a prefix this is
+// TileCursor.
+template <bool PREFIX>
+struct SegmentCursor {
+  const int32_t* cols;
+  Layout<PREFIX> L;
+  int e = 0, kt = 0, kf = 0, tiles = 0;
+  __device__ __forceinline__ void start(const int32_t* c, Layout<PREFIX> lay) {
+    cols = c;
+    L = lay;
+    e = 0;
+    kt = 0;
+    kf = cols[0];
+    tiles = (L.len(kf) + kBlockK - 1) / kBlockK;
+  }
+  __device__ __forceinline__ void advance(int n_segments) {
+    if (++kt == tiles) {
+      kt = 0;
+      if (++e < n_segments) {
+        kf = cols[e];
+        tiles = (L.len(kf) + kBlockK - 1) / kBlockK;
+      }
+    }
+  }
+  __device__ __forceinline__ size_t key0() const { return (size_t)L.start(kf) + kt * kBlockK; }
+  __device__ __forceinline__ int nvalid() const { return min(kBlockK, L.len(kf) - kt * kBlockK); }
+};
+
+template <int D, bool PREFIX>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
     const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int H,
-    int F, int T, int nqb, uint32_t n_wg, float* __restrict__ ws_o, float* __restrict__ ws_lse,
-    float* __restrict__ lse, float c, uint32_t qflip, uint32_t qmask) {
+    int F, int T, int P, int nqb, uint32_t n_wg, float* __restrict__ ws_o,
+    float* __restrict__ ws_lse, float* __restrict__ lse, float c, uint32_t qflip, uint32_t qmask) {
   using Sh = Shape<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
@@ -264,8 +312,13 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   const int n_kept = item[3];
   const int slot = item[4];  // >= 0: a piece of a split frame, written as a partial
   const int qb = (int)(rem % nqb);
+  const Layout<PREFIX> lay{F, T, P};
+  const int seg0 = lay.start(frame), seg_len = lay.len(frame);
+  // With a prefix the text segment is shorter than the grid's query blocks assume.
+  if (PREFIX && qb * kBlockQ >= seg_len) return;
 
-  const size_t head_elems = (size_t)F * T * D;
+  const size_t head_rows = (size_t)P * PREFIX + (size_t)F * T;
+  const size_t head_elems = head_rows * D;
   const uint16_t* Qh = Q + bh * head_elems;
   const uint16_t* Kh = K + bh * head_elems;
   const uint16_t* Vh = V + bh * head_elems;
@@ -279,16 +332,16 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   // and their Q^T B-operand slices.
   const int qrow0 = qb * kBlockQ + wave * kWaveQ + n;
   // Waves whose rows all lie past the frame end only help load tiles.
-  const bool wave_active = qb * kBlockQ + wave * kWaveQ < T;
+  const bool wave_active = qb * kBlockQ + wave * kWaveQ < seg_len;
   bf16x8 qf[2][Sh::kChunks];
 #pragma unroll
   for (int qs = 0; qs < 2; ++qs) {
     const int qrow = qrow0 + 32 * qs;
-    const uint16_t* qp = Qh + ((size_t)frame * T + qrow) * D + 8 * hf;
+    const uint16_t* qp = Qh + ((size_t)seg0 + qrow) * D + 8 * hf;
 #pragma unroll
     for (int cc = 0; cc < Sh::kChunks; ++cc) {
       u32x4 x = {0u, 0u, 0u, 0u};
-      if (qrow < T) x = (load16(qp + 16 * cc) & qmask) ^ qflip;
+      if (qrow < seg_len) x = (load16(qp + 16 * cc) & qmask) ^ qflip;
       qf[qs][cc] = as_bf16x8(x);
     }
   }
@@ -305,7 +358,11 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   const float lazy = exp2f(kLazyLog2);
 
   const int tpf = (T + kBlockK - 1) / kBlockK;
-  const int n_tiles = n_kept * tpf;
+  int n_tiles = n_kept * tpf;
+  if constexpr (PREFIX) {
+    // the text segment (index F) sorts last in a kept list
+    if (n_kept > 0 && cols[kbeg + n_kept - 1] == F) n_tiles += (P + kBlockK - 1) / kBlockK - tpf;
+  }
 
   if (n_tiles > 0) {
     TileLoader<D, true> kl;
@@ -316,8 +373,8 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     VAddr<D> va;
     ka.init(n, hf);
     va.init(lane);
-    TileCursor cur, nxt;  // tile t (being consumed) and tile t+1 (being loaded)
-    cur.start(cols + kbeg, tpf, T);
+    SegmentCursor<PREFIX> cur, nxt;  // tile t (being consumed) and tile t+1 (being loaded)
+    cur.start(cols + kbeg, lay);
     kl.load(Kh, cur.key0(), cur.nvalid(), sK[0], wave);
     vl.load(Vh, cur.key0(), cur.nvalid(), sV[0], wave);
     nxt = cur;
@@ -399,10 +456,10 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   for (int qs = 0; qs < 2; ++qs) {
     const float l_tot = pair_sum(l_run[qs]);
     const int qrow = qrow0 + 32 * qs;
-    if (qrow < T) {
+    if (qrow < seg_len) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       if (slot < 0) {
-        uint16_t* op = Oh + ((size_t)frame * T + qrow) * D;
+        uint16_t* op = Oh + ((size_t)seg0 + qrow) * D;
 #pragma unroll
         for (int mb = 0; mb < Sh::kDBlocks; ++mb)
 #pragma unroll
@@ -413,12 +470,13 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
             *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
           }
         if (lse && hf == 0)
-          lse[((size_t)bh * F + frame) * T + qrow] =
+          lse[(size_t)bh * head_rows + seg0 + qrow] =
               l_tot > 0.f ? (m_ref[qs] * c + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f
                           : -INFINITY;
       } else {
         const uint32_t nb = n_wg / per_b;  // batch size
-        const size_t prow = ((size_t)slot * nb + b) * T + qrow;
+        const int slot_rows = PREFIX ? max(T, P) : T;  // rows per (slot, batch entry)
+        const size_t prow = ((size_t)slot * nb + b) * slot_rows + qrow;
         float* op = ws_o + prow * D;
 #pragma unroll
         for (int mb = 0; mb < Sh::kDBlocks; ++mb)
@@ -434,26 +492,32 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   }
 }
 
-// Combines the pieces of split query frames. One thread per (split frame, batch
-// entry, query row, 8 consecutive d): with M the largest piece log-sum-exp,
-// out = sum_p 2^(lse_p - M) (O/l)_p / sum_p 2^(lse_p - M), rounded to bf16 (RNE);
-// the row's log-sum-exp is M + log2(sum_p 2^(lse_p - M)), stored in natural log.
+// Combines the pieces of split query frames (or of the split text segment of the
+// MM-DiT form). One thread per (split segment, batch entry, row, 8 consecutive d):
+// with M the largest piece log-sum-exp, out = sum_p 2^(lse_p - M) (O/l)_p /
+// sum_p 2^(lse_p - M), rounded to bf16 (RNE); the row's log-sum-exp is
+// M + log2(sum_p 2^(lse_p - M)), stored in natural log. Partials are laid out
+// [slot][batch][L][d] with L = max(T, P) rows per slot.
 template <int D>
 __global__ __launch_bounds__(256) void merge_partials_kernel(
     const float* __restrict__ ws_o, const float* __restrict__ ws_lse,
-    const int32_t* __restrict__ heavy, int n_heavy, int B, int H, int F, int T,
+    const int32_t* __restrict__ heavy, int n_heavy, int B, int H, int F, int T, int P,
     uint16_t* __restrict__ O, float* __restrict__ lse) {
   constexpr int kGroups = D / 8;
+  const int L = max(T, P);
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t per_frame = (size_t)B * T * kGroups;
-  if (idx >= per_frame * (size_t)n_heavy) return;
-  const int hv = (int)(idx / per_frame);
-  const size_t r = idx - (size_t)hv * per_frame;
+  const size_t per_seg = (size_t)B * L * kGroups;
+  if (idx >= per_seg * (size_t)n_heavy) return;
+  const int hv = (int)(idx / per_seg);
+  const size_t r = idx - (size_t)hv * per_seg;
   const int grp = (int)(r % kGroups);
-  const size_t row = r / kGroups;  // b * T + t
+  const size_t row = r / kGroups;  // b * L + t
+  const size_t b = row / L, t = row - b * L;
   const int head = heavy[4 * hv], frame = heavy[4 * hv + 1];
   const int slot0 = heavy[4 * hv + 2], np = heavy[4 * hv + 3];
-  const size_t slot_stride = (size_t)B * T;
+  const int seg0 = frame < F ? P + frame * T : 0, seg_len = frame < F ? T : P;
+  if ((int)t >= seg_len) return;
+  const size_t slot_stride = (size_t)B * L;
   float mx = -INFINITY;
   for (int p = 0; p < np; ++p) mx = fmaxf(mx, ws_lse[(size_t)(slot0 + p) * slot_stride + row]);
   f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
@@ -467,8 +531,7 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(
     wsum += w;
   }
   const float inv = 1.f / wsum;
-  const size_t b = row / T, t = row - b * T;
-  const size_t orow = ((b * H + head) * F + frame) * (size_t)T + t;
+  const size_t orow = (b * H + head) * ((size_t)P + (size_t)F * T) + seg0 + t;
   const f32x8 x = {a0[0] * inv, a0[1] * inv, a0[2] * inv, a0[3] * inv,
                    a1[0] * inv, a1[1] * inv, a1[2] * inv, a1[3] * inv};
   *reinterpret_cast<bf16x8*>(O + orow * D + 8 * grp) = __builtin_convertvector(x, bf16x8);
@@ -477,19 +540,24 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(
 
 template <int D>
 hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
-  const int nqb = (a.T + kBlockQ - 1) / kBlockQ;
-  hipLaunchKernelGGL(tile_attn_fwd_kernel<D>, dim3(a.n_wg), dim3(kThreads), 0, stream, a.q, a.k,
-                     a.v, a.out, a.items, a.cols, a.n_items, a.H, a.F, a.T, nqb, a.n_wg, a.ws_o,
-                     a.ws_lse, a.lse, a.c, a.qflip, a.qmask);
+  const int nqb = (std::max(a.T, a.P) + kBlockQ - 1) / kBlockQ;
+  if (a.P > 0)
+    hipLaunchKernelGGL((tile_attn_fwd_kernel<D, true>), dim3(a.n_wg), dim3(kThreads), 0, stream, a.q,
+                       a.k, a.v, a.out, a.items, a.cols, a.n_items, a.H, a.F, a.T, a.P, nqb, a.n_wg,
+                       a.ws_o, a.ws_lse, a.lse, a.c, a.qflip, a.qmask);
+  else
+    hipLaunchKernelGGL((tile_attn_fwd_kernel<D, false>), dim3(a.n_wg), dim3(kThreads), 0, stream,
+                       a.q, a.k, a.v, a.out, a.items, a.cols, a.n_items, a.H, a.F, a.T, 0, nqb,
+                       a.n_wg, a.ws_o, a.ws_lse, a.lse, a.c, a.qflip, a.qmask);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_merge_d(const MergeArgs& a, hipStream_t stream) {
-  const size_t threads = (size_t)a.n_heavy * a.B * a.T * (D / 8);
+  const size_t threads = (size_t)a.n_heavy * a.B * std::max(a.T, a.P) * (D / 8);
   const size_t blocks = (threads + 255) / 256;
   hipLaunchKernelGGL(merge_partials_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.ws_o,
-                     a.ws_lse, a.heavy, a.n_heavy, a.B, a.H, a.F, a.T, a.out, a.lse);
+                     a.ws_lse, a.heavy, a.n_heavy, a.B, a.H, a.F, a.T, a.P, a.out, a.lse);
   return hipGetLastError();
 }
 

@@ -203,3 +203,22 @@ def test_bwd_argument_errors_before_any_gpu_call():
     assert _bwd(dv=(5 << 12) + 16) == 7  # dv overlaps dout
     assert _bwd(lse=(7 << 12) + 64) == 7  # dq overlaps lse
     assert "lse" in lib.tile_attn_last_error().decode()
+
+
+def _mmdit(q=1 << 13, k=2 << 13, v=3 << 13, out=4 << 13, B=1, H=2, F=2, T=8, P=5, d=64, masks=None,
+           n=None, lse=None, scale=0.125):
+    # each tensor of B=1, H=2, P + F*T = 21 tokens, d=64 spans 5376 bytes < 8 KiB
+    m = np.ones((H, F, F), np.uint8) if masks is None else masks
+    nm = m.size // (F * F) if n is None else n
+    return lib.tile_attn_fwd_mmdit(q, k, v, out, B, H, F, T, P, d, m.ctypes.data, nm, scale, lse, None)
+
+
+def test_mmdit_argument_errors_before_any_gpu_call():
+    assert _mmdit(P=-1) == 2 and _mmdit(B=0) == 2 and _mmdit(d=80) == 3
+    assert _mmdit(n=3) == 4
+    assert lib.tile_attn_fwd_mmdit(1 << 13, 2 << 13, 3 << 13, 4 << 13, 1, 2, 2, 8, 5, 64, None, 2, 0.1,
+                                   None, None) == 1
+    assert _mmdit(out=(3 << 13) + 4096) == 7  # out overlaps v within P + F*T tokens
+    assert _mmdit(lse=(1 << 20) | 2) == 5
+    assert _mmdit(lse=(2 << 13) + 5000) == 7  # lse overlaps k's last rows
+    assert _mmdit(T=2 ** 30, F=2, P=2 ** 30) == 2  # P + F*T overflows

@@ -21,7 +21,8 @@ import numpy as np
 
 @dataclasses.dataclass(frozen=True)
 class Workload:
-    """One attention problem: [B, H, F*T, d] bf16 tensors plus a mask recipe."""
+    """One attention problem: [B, H, prefix + F*T, d] bf16 tensors plus a mask recipe
+    (prefix = text tokens before the video in the MM-DiT form, else 0)."""
 
     name: str
     B: int
@@ -32,10 +33,11 @@ class Workload:
     g: int  # number of global reference frames in the k:(F-k) mask
     dist: str = "iid"  # "iid" or "frame_shift"
     seed: int = 0
+    prefix: int = 0
 
     @property
     def S(self) -> int:
-        return self.F * self.T
+        return self.prefix + self.F * self.T
 
     def scale(self) -> float:
         return 1.0 / float(np.sqrt(self.d))
@@ -55,6 +57,9 @@ WORKLOADS = {
     "sp_share": Workload("sp_share", B=1, H=6, F=24, T=3600, d=96, g=1),
     # Long horizon: 48 latent frames of a 30 x 40 grid.
     "long": Workload("long", B=1, H=24, F=48, T=1200, d=96, g=2),
+    # MM-DiT form at the CogVideoX-5B shape of App. E: 49 frames -> 13 latent frames,
+    # 480p -> 30 x 45 = 1350 tokens per frame, 226 text tokens first, 48 heads of 64.
+    "cog": Workload("cog", B=1, H=48, F=13, T=1350, d=64, g=1, prefix=226),
 }
 
 
@@ -77,8 +82,9 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     return (b.astype(np.uint32) << 16).view(np.float32)
 
 
-def make_qkv(B: int, H: int, F: int, T: int, d: int, seed: int = 0, dist: str = "iid"):
-    """Draw Q, K, V as bf16 bit patterns of shape [B, H, F*T, d].
+def make_qkv(B: int, H: int, F: int, T: int, d: int, seed: int = 0, dist: str = "iid",
+             prefix: int = 0):
+    """Draw Q, K, V as bf16 bit patterns of shape [B, H, prefix + F*T, d].
 
     iid: every element is N(0, 1).
     frame_shift: x = z + 0.5 * mu, with z ~ N(0, 1) per element and one
@@ -86,21 +92,22 @@ def make_qkv(B: int, H: int, F: int, T: int, d: int, seed: int = 0, dist: str = 
     mean, which mimics frame-correlated video tokens.
 
     One numpy PCG64 stream seeded with ``seed`` draws Q, K, V in that order,
-    then (frame_shift only) the shifts for Q, K, V in that order.
+    then (frame_shift only) the shifts for Q, K, V in that order. Text tokens
+    (the first ``prefix``) are iid N(0, 1) and get no frame shift.
     """
     rng = np.random.default_rng(seed)
-    S = F * T
+    S = prefix + F * T
     outs = []
     for _ in range(3):
         outs.append(rng.standard_normal((B, H, S, d), dtype=np.float32))
     if dist == "frame_shift":
         for x in outs:
             mu = rng.standard_normal((B, H, F, 1, d), dtype=np.float32)
-            x.reshape(B, H, F, T, d)[...] += np.float32(0.5) * mu
+            x[:, :, prefix:].reshape(B, H, F, T, d)[...] += np.float32(0.5) * mu
     elif dist != "iid":
         raise ValueError(f"unknown distribution {dist!r}")
     return tuple(f32_to_bf16_bits(x) for x in outs)
 
 
 def make_workload_qkv(w: Workload):
-    return make_qkv(w.B, w.H, w.F, w.T, w.d, seed=w.seed, dist=w.dist)
+    return make_qkv(w.B, w.H, w.F, w.T, w.d, seed=w.seed, dist=w.dist, prefix=w.prefix)
