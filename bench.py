@@ -50,9 +50,12 @@ def log(*a):
 
 def kept_flop(w, nnz: int, which: str = "fwd") -> float:
     """Forward: QK^T and PV over kept tiles only, 4 * B * H * d * T^2 per kept tile.
-    Backward: the five products of the gradients, 10 * B * H * d * T^2 per kept tile."""
+    Backward: the five products of the gradients, 10 * B * H * d * T^2 per kept tile.
+    With a text prefix of P tokens (MM-DiT form) every query also attends the text and
+    the text queries attend everything: 4 * B * H * d * (T^2 nnz + F T P + P S)."""
     per = 4.0 if which == "fwd" else 10.0
-    return per * w.B * w.H * w.d * float(w.T) ** 2 * nnz
+    pairs = float(w.T) ** 2 * nnz + float(w.prefix) * (w.F * w.T + w.S)
+    return per * w.B * w.H * w.d * pairs
 
 
 def time_calls(fn, steps: int, warmup: int, torch):
@@ -110,14 +113,19 @@ def cpu_baseline(w, qb, kb, vb, mask, budget_s: float):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
+    from oracle import mmdit as ommd
+
     nnz = int(np.count_nonzero(mask))
     done, t0 = 0, time.perf_counter()
     while done < w.H and time.perf_counter() - t0 < budget_s:
         sl = slice(done, done + 1)
-        oa.attention(qb[:, sl], kb[:, sl], vb[:, sl], mask, w.T, w.scale())
+        if w.prefix:
+            ommd.attention_mmdit(qb[:, sl], kb[:, sl], vb[:, sl], mask, w.T, w.prefix, w.scale())
+        else:
+            oa.attention(qb[:, sl], kb[:, sl], vb[:, sl], mask, w.T, w.scale())
         done += 1
     dt = time.perf_counter() - t0
-    flop = 4.0 * w.B * done * w.d * float(w.T) ** 2 * nnz
+    flop = kept_flop(w, nnz) * done / w.H
     return {
         "value": flop / dt / 1e12,
         "unit": "TFLOP/s",
@@ -178,15 +186,20 @@ class Problem:
         if which == "bwd":
             self.gb = make_grad_bits(w)
             self.dout = dev(self.gb)
-            self.lse = torch.empty((w.B, w.H, w.F * w.T), dtype=torch.float32, device="cuda")
+            self.lse = torch.empty((w.B, w.H, w.S), dtype=torch.float32, device="cuda")
             self.grads = [torch.empty_like(self.q) for _ in range(3)]
         self.stream = torch.cuda.current_stream()
 
     def step_fn(self, mask):
         w, ta, st = self.w, self.ta, self.stream
         q, k, v, out = self.q, self.k, self.v, self.out
+        if self.which == "fwd" and w.prefix:
+            return lambda: ta.tile_attn_fwd_mmdit(q, k, v, out, w.B, w.H, w.F, w.T, w.prefix, w.d, mask,
+                                                  w.scale(), None, st)
         if self.which == "fwd":
             return lambda: ta.tile_attn_fwd(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), st)
+        if w.prefix:
+            raise SystemExit("the gradients of the MM-DiT form are not implemented")
         # out and lse of this mask, once, outside the timed region
         ta.tile_attn_fwd_heads(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), self.lse, st)
         dq, dk, dv = self.grads
@@ -226,6 +239,10 @@ ALL_CASES = [
     ("sweep", "sym", 2), ("sweep", "sym", 4), ("sweep", "sym", 8),
     ("sp_share", "col", 1), ("sp_share", "sym", 1),
     ("long", "col", 2), ("long", "sym", 2),
+    # MM-DiT form at the CogVideoX-5B shape: tab:cog_kernel labels 12, 6, 4, 3, 2, 1 are
+    # k = 1, 2, 3, 4, 6, 12 global frames (sym form).
+    ("cog", "sym", 1), ("cog", "sym", 2), ("cog", "sym", 3), ("cog", "sym", 4),
+    ("cog", "sym", 6), ("cog", "sym", 12),
 ]
 
 
