@@ -239,6 +239,7 @@ ALL_CASES = [
     ("sweep", "sym", 2), ("sweep", "sym", 4), ("sweep", "sym", 8),
     ("sp_share", "col", 1), ("sp_share", "sym", 1),
     ("long", "col", 2), ("long", "sym", 2),
+    ("93f_d128", "col", 1), ("93f_d128", "sym", 1),
     # MM-DiT form at the CogVideoX-5B shape: tab:cog_kernel labels 12, 6, 4, 3, 2, 1 are
     # k = 1, 2, 3, 4, 6, 12 global frames (sym form).
     ("cog", "sym", 1), ("cog", "sym", 2), ("cog", "sym", 3), ("cog", "sym", 4),

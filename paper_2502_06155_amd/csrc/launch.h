@@ -5,9 +5,11 @@
 
 namespace ta {
 
-// Query rows per workgroup; each of the four waves owns 64 query rows.
-constexpr int kBlockQ = 256;
 constexpr int kThreads = 256;
+
+// Query rows per forward workgroup for head dimension d (4 waves of 64 rows, or of 32
+// rows at d = 128).
+int fwd_rows_per_workgroup(int d);
 
 struct FwdArgs {
   const uint16_t* q;
@@ -32,7 +34,7 @@ struct FwdArgs {
   float c;              // > 0: |scale| * log2(e), logits in base-2 units
   uint32_t qflip;       // 0x80008000 flips the sign of q (negative scale), else 0
   uint32_t qmask;       // 0 zeroes q (scale 0: exactly uniform weights), else ~0
-  uint32_t n_wg;        // B * n_items * ceil(max(T, P) / kBlockQ)
+  uint32_t n_wg;        // B * n_items * ceil(max(T, P) / fwd_rows_per_workgroup(d))
 };
 
 // Combines the partial results of split query frames: heavy holds 4 int32 per split

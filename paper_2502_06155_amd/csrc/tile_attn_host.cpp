@@ -138,7 +138,8 @@ int check_args(const void* q, const void* k, const void* v, void* out, int B, in
   if (F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F exceeds TA_MAX_FRAMES");
   if ((int64_t)F * T + P > INT32_MAX) return fail(TA_ERR_BAD_SHAPE, "P + F * T exceeds 2^31 - 1");
   if (d != 64 && d != 96 && d != 128) return fail(TA_ERR_HEAD_DIM, "d must be 64, 96 or 128");
-  const int64_t nqb = (std::max(T, P) + ta::kBlockQ - 1) / ta::kBlockQ;
+  const int rows = ta::fwd_rows_per_workgroup(d) > 0 ? ta::fwd_rows_per_workgroup(d) : 256;
+  const int64_t nqb = (std::max(T, P) + rows - 1) / rows;
   const int64_t n_wg = (int64_t)B * H * (F + (P > 0)) * nqb;
   if (n_wg * ta::kThreads > (int64_t)UINT32_MAX)
     return fail(TA_ERR_BAD_SHAPE, "B * H * F * ceil(T / 256) workgroups exceed the grid limit");
@@ -242,7 +243,7 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
   const int L = std::max(T, P);  // longest segment: rows per query-block grid column
-  const int64_t nqb = (L + ta::kBlockQ - 1) / ta::kBlockQ;
+  const int64_t nqb = (L + ta::fwd_rows_per_workgroup(d) - 1) / ta::fwd_rows_per_workgroup(d);
   // With a text prefix, plan F + 1 segments: video row i keeps its mask row plus the
   // text (segment F); the text row keeps everything.
   std::vector<uint8_t> aug;

@@ -60,9 +60,14 @@ namespace ta {
 namespace {
 
 constexpr int kWaves = kThreads / 64;
-constexpr int kWaveQ = 64;   // query rows per wave: two 32-query column blocks
 constexpr float kLazyLog2 = 10.f;
-static_assert(kWaves * kWaveQ == kBlockQ, "workgroup rows");
+// 32-query column blocks per wave: two (64 rows, every LDS fragment feeds two MFMAs)
+// where they fit 256 VGPRs, one at d = 128 (two spilled some 70 VGPRs inside the
+// tile loop and ran at half the rate).
+template <int D>
+constexpr int fwd_q_blocks() { return D == 128 ? 1 : 2; }
+template <int D>
+constexpr int fwd_rows_per_wg() { return kWaves * 32 * fwd_q_blocks<D>(); }
 
 template <int D>
 struct Shape {
@@ -163,18 +168,18 @@ struct VAddr {
 
 // S^T of 32-key block kb of a K tile for both 32-query column blocks of the wave
 // (32 keys x 32 queries each), raw logits. Each K fragment feeds two MFMAs.
-template <int D>
-__device__ __forceinline__ void qk_block(const uint16_t* sK, const bf16x8 (&qf)[2][D / 16],
-                                         const KAddr<D>& ka, int kb, f32x16 (&s)[2]) {
+template <int D, int QB>
+__device__ __forceinline__ void qk_block(const uint16_t* sK, const bf16x8 (&qf)[QB][D / 16],
+                                         const KAddr<D>& ka, int kb, f32x16 (&s)[QB]) {
   const uint16_t* base = sK + kb * 32 * D;
   const bf16x8 a0 = as_bf16x8(load16(base + ka.at[0]));
-  s[0] = mfma32(a0, qf[0][0], f32x16{});
-  s[1] = mfma32(a0, qf[1][0], f32x16{});
+#pragma unroll
+  for (int qs = 0; qs < QB; ++qs) s[qs] = mfma32(a0, qf[qs][0], f32x16{});
 #pragma unroll
   for (int cc = 1; cc < D / 16; ++cc) {
     const bf16x8 a = as_bf16x8(load16(base + ka.at[cc]));
-    s[0] = mfma32(a, qf[0][cc], s[0]);
-    s[1] = mfma32(a, qf[1][cc], s[1]);
+#pragma unroll
+    for (int qs = 0; qs < QB; ++qs) s[qs] = mfma32(a, qf[qs][cc], s[qs]);
   }
 }
 
@@ -202,16 +207,16 @@ __device__ __forceinline__ bf16x8 vt_frag(const uint16_t* sV, const VAddr<D>& va
 
 // O^T (d x 32 queries, both column blocks) += V^T * P^T over 32-key block kb (key
 // chunks 2kb, 2kb+1). Each V^T fragment feeds two MFMAs.
-template <int D>
-__device__ __forceinline__ void pv_block(const uint16_t* sV, const bf16x8 (&p)[2][2],
-                                         const VAddr<D>& va, int kb, f32x16 (&o)[2][D / 32]) {
+template <int D, int QB>
+__device__ __forceinline__ void pv_block(const uint16_t* sV, const bf16x8 (&p)[QB][2],
+                                         const VAddr<D>& va, int kb, f32x16 (&o)[QB][D / 32]) {
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
     for (int mb = 0; mb < D / 32; ++mb) {
       const bf16x8 a = vt_frag<D>(sV, va, mb, 2 * kb + c2);
-      o[0][mb] = mfma32(a, p[0][c2], o[0][mb]);
-      o[1][mb] = mfma32(a, p[1][c2], o[1][mb]);
+#pragma unroll
+      for (int qs = 0; qs < QB; ++qs) o[qs][mb] = mfma32(a, p[qs][c2], o[qs][mb]);
     }
 }
 
@@ -298,6 +303,9 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     int F, int T, int P, int nqb, uint32_t n_wg, float* __restrict__ ws_o,
     float* __restrict__ ws_lse, float* __restrict__ lse, float c, uint32_t qflip, uint32_t qmask) {
   using Sh = Shape<D>;
+  constexpr int QB = fwd_q_blocks<D>();
+  constexpr int kWaveQ = 32 * QB;
+  constexpr int kBlockQ = fwd_rows_per_wg<D>();
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
 
@@ -333,9 +341,9 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   const int qrow0 = qb * kBlockQ + wave * kWaveQ + n;
   // Waves whose rows all lie past the frame end only help load tiles.
   const bool wave_active = qb * kBlockQ + wave * kWaveQ < seg_len;
-  bf16x8 qf[2][Sh::kChunks];
+  bf16x8 qf[QB][Sh::kChunks];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < QB; ++qs) {
     const int qrow = qrow0 + 32 * qs;
     const uint16_t* qp = Qh + ((size_t)seg0 + qrow) * D + 8 * hf;
 #pragma unroll
@@ -346,15 +354,19 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     }
   }
 
-  f32x16 o[2][Sh::kDBlocks];
+  f32x16 o[QB][Sh::kDBlocks];
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs)
+  for (int qs = 0; qs < QB; ++qs)
 #pragma unroll
     for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[qs][mb] = f32x16{};
   // Per column block: exponent reference (raw logit units) of this lane's query
   // and this lane's part of the running sum of weights.
-  float m_ref[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
+  float m_ref[QB], l_run[QB];
+#pragma unroll
+  for (int qs = 0; qs < QB; ++qs) {
+    m_ref[qs] = -INFINITY;
+    l_run[qs] = 0.f;
+  }
   const float lazy = exp2f(kLazyLog2);
 
   const int tpf = (T + kBlockK - 1) / kBlockK;
@@ -387,10 +399,13 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     // block m_ref = -inf turns masked keys into NaN weights) the references are
     // raised to cover the block, what is accumulated so far is rescaled, and the
     // block's weights are redone. Then the block's sums join the running sums.
-    auto check_block = [&](const f32x16(&s)[2], bf16x8(&p)[2][2], float(&ls)[2]) {
-      if (__builtin_amdgcn_ballot_w64(!(ls[0] <= lazy && ls[1] <= lazy)) != 0) {
+    auto check_block = [&](const f32x16(&s)[QB], bf16x8(&p)[QB][2], float(&ls)[QB]) {
+      bool small = true;
 #pragma unroll
-        for (int qs = 0; qs < 2; ++qs) {
+      for (int qs = 0; qs < QB; ++qs) small = small && ls[qs] <= lazy;
+      if (__builtin_amdgcn_ballot_w64(!small) != 0) {
+#pragma unroll
+        for (int qs = 0; qs < QB; ++qs) {
           const float m_new = fmaxf(m_ref[qs], pair_max(block_max(s[qs])));
           const float alpha = fast_exp2((m_ref[qs] - m_new) * c);
           l_run[qs] *= alpha;
@@ -400,8 +415,8 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
           ls[qs] = block_weights(s[qs], c, m_new * c, p[qs]);
         }
       }
-      l_run[0] += ls[0];
-      l_run[1] += ls[1];
+#pragma unroll
+      for (int qs = 0; qs < QB; ++qs) l_run[qs] += ls[qs];
     };
 
     for (int t = 0; t < n_tiles; ++t) {
@@ -417,29 +432,29 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
         // Within the tile: QK^T of block 1 runs on the matrix cores while the
         // weights of block 0 form on the vector ALUs, then PV of block 0 while the
         // weights of block 1 form, then PV of block 1.
-        f32x16 s0[2], s1[2];
-        bf16x8 p0[2][2], p1[2][2];
-        float l0[2], l1[2];
-        qk_block<D>(sK[buf], qf, ka, 0, s0);
+        f32x16 s0[QB], s1[QB];
+        bf16x8 p0[QB][2], p1[QB][2];
+        float l0[QB], l1[QB];
+        qk_block<D, QB>(sK[buf], qf, ka, 0, s0);
         if (nvalid < kBlockK) {
-          mask_tail(s0[0], 0, hf, nvalid);
-          mask_tail(s0[1], 0, hf, nvalid);
-        }
-        qk_block<D>(sK[buf], qf, ka, 1, s1);
 #pragma unroll
-        for (int qs = 0; qs < 2; ++qs) l0[qs] = block_weights(s0[qs], c, m_ref[qs] * c, p0[qs]);
-        interleave_mfma_valu<2 * (D / 16), 48>();
+          for (int qs = 0; qs < QB; ++qs) mask_tail(s0[qs], 0, hf, nvalid);
+        }
+        qk_block<D, QB>(sK[buf], qf, ka, 1, s1);
+#pragma unroll
+        for (int qs = 0; qs < QB; ++qs) l0[qs] = block_weights(s0[qs], c, m_ref[qs] * c, p0[qs]);
+        interleave_mfma_valu<QB * (D / 16), 24 * QB>();
         check_block(s0, p0, l0);
         if (nvalid < kBlockK) {
-          mask_tail(s1[0], 1, hf, nvalid);
-          mask_tail(s1[1], 1, hf, nvalid);
-        }
-        pv_block<D>(sV[buf], p0, va, 0, o);
 #pragma unroll
-        for (int qs = 0; qs < 2; ++qs) l1[qs] = block_weights(s1[qs], c, m_ref[qs] * c, p1[qs]);
-        interleave_mfma_valu<2 * (D / 16), 48>();
+          for (int qs = 0; qs < QB; ++qs) mask_tail(s1[qs], 1, hf, nvalid);
+        }
+        pv_block<D, QB>(sV[buf], p0, va, 0, o);
+#pragma unroll
+        for (int qs = 0; qs < QB; ++qs) l1[qs] = block_weights(s1[qs], c, m_ref[qs] * c, p1[qs]);
+        interleave_mfma_valu<QB * (D / 16), 24 * QB>();
         check_block(s1, p1, l1);
-        pv_block<D>(sV[buf], p1, va, 1, o);
+        pv_block<D, QB>(sV[buf], p1, va, 1, o);
       }
       cur = nxt;
       nxt.advance(n_kept);
@@ -453,7 +468,7 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   // log2(sum_t 2^(c s_t)) = c m_ref + log2(l) for the merge. 4 consecutive d per
   // access.
 #pragma unroll
-  for (int qs = 0; qs < 2; ++qs) {
+  for (int qs = 0; qs < QB; ++qs) {
     const float l_tot = pair_sum(l_run[qs]);
     const int qrow = qrow0 + 32 * qs;
     if (qrow < seg_len) {
@@ -540,7 +555,7 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(
 
 template <int D>
 hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
-  const int nqb = (std::max(a.T, a.P) + kBlockQ - 1) / kBlockQ;
+  const int nqb = (std::max(a.T, a.P) + fwd_rows_per_wg<D>() - 1) / fwd_rows_per_wg<D>();
   if (a.P > 0)
     hipLaunchKernelGGL((tile_attn_fwd_kernel<D, true>), dim3(a.n_wg), dim3(kThreads), 0, stream, a.q,
                        a.k, a.v, a.out, a.items, a.cols, a.n_items, a.H, a.F, a.T, a.P, nqb, a.n_wg,
@@ -562,6 +577,15 @@ hipError_t launch_merge_d(const MergeArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+int fwd_rows_per_workgroup(int d) {
+  switch (d) {
+    case 64: return fwd_rows_per_wg<64>();
+    case 96: return fwd_rows_per_wg<96>();
+    case 128: return fwd_rows_per_wg<128>();
+    default: return 0;
+  }
+}
 
 hipError_t launch_merge_partials(const MergeArgs& a, hipStream_t stream) {
   switch (a.d) {

@@ -208,6 +208,7 @@ FULL_CASES = [
     ("sweep", "col", 2), ("sweep", "sym", 2), ("sweep", "col", 4), ("sweep", "sym", 8),
     ("sweep", "dense", 1),
     ("sp_share", "col", 1), ("long", "col", 2), ("long", "sym", 2),
+    ("93f_d128", "col", 1), ("93f_d128", "sym", 1),
 ]
 
 

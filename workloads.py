@@ -57,6 +57,8 @@ WORKLOADS = {
     "sp_share": Workload("sp_share", B=1, H=6, F=24, T=3600, d=96, g=1),
     # Long horizon: 48 latent frames of a 30 x 40 grid.
     "long": Workload("long", B=1, H=24, F=48, T=1200, d=96, g=2),
+    # The 93-frame shape with 128-wide heads (18 heads keep the model width of 24 x 96).
+    "93f_d128": Workload("93f_d128", B=1, H=18, F=24, T=3600, d=128, g=1),
     # MM-DiT form at the CogVideoX-5B shape of App. E: 49 frames -> 13 latent frames,
     # 480p -> 30 x 45 = 1350 tokens per frame, 226 text tokens first, 48 heads of 64.
     "cog": Workload("cog", B=1, H=48, F=13, T=1350, d=64, g=1, prefix=226),
