@@ -112,3 +112,81 @@ def attention_mmdit_lse(q, k, mask, T: int, P: int, scale: float) -> np.ndarray:
                 m = logits.max(axis=-1, keepdims=True)
                 lse[b, h, rows] = (m + np.log(np.exp(logits - m).sum(axis=-1, keepdims=True)))[:, 0]
     return lse
+
+
+def attention_backward_mmdit(q, k, v, dout, mask, T: int, P: int, scale: float):
+    """Gradients (dq, dk, dv), float64 [B, H, P + F*T, d], of ``attention_mmdit`` for the
+    upstream gradient dout: the chain rule through each query's softmax over its keys,
+    dS = P (dP - delta) with dP = dO V^T and delta = <dO, out>; dq = scale dS K,
+    dk = scale dS^T Q, dv = P^T dO (sums over the query-key pairs the form keeps)."""
+    mask = np.asarray(mask)
+    B, H, S, d, F = _shape(q, T, P, mask)
+    dq, dk, dv = (np.zeros((B, H, S, d)) for _ in range(3))
+    for b in range(B):
+        for h in range(H):
+            qh, kh, vh, gh = (as_f64(x[b, h]) for x in (q, k, v, dout))
+            mh = head_mask(mask, h)
+            for i, rows in _query_groups(F, T, P):
+                cols = key_tokens(mh, i, T, P)
+                if cols.size == 0:
+                    continue
+                logits = scale * (qh[rows] @ kh[cols].T)
+                w = np.exp(logits - logits.max(axis=-1, keepdims=True))
+                p = w / w.sum(axis=-1, keepdims=True)
+                out = p @ vh[cols]
+                ds = p * (gh[rows] @ vh[cols].T - (gh[rows] * out).sum(axis=-1, keepdims=True))
+                dq[b, h, rows] += scale * (ds @ kh[cols])
+                dk[b, h, cols] += scale * (ds.T @ qh[rows])
+                dv[b, h, cols] += p.T @ gh[rows]
+    return dq, dk, dv
+
+
+def attention_backward_mmdit_rows(q, k, v, dout, mask, T: int, P: int, scale: float, bq, hq, sq,
+                                  bk, hk, sk, chunk: int = 512):
+    """``attention_backward_mmdit`` at chosen rows only: dq at query tokens (bq, hq, sq)
+    and dk, dv at key tokens (bk, hk, sk), float64 [n, d]; a key's gradient sums over
+    every query whose key set holds it, ``chunk`` query rows at a time."""
+    mask = np.asarray(mask)
+    B, H, S, d, F = _shape(q, T, P, mask)
+    dq = np.zeros((len(sq), d))
+    dk = np.zeros((len(sk), d))
+    dv = np.zeros((len(sk), d))
+    bq, hq, sq, bk, hk, sk = (np.asarray(x, dtype=np.int64) for x in (bq, hq, sq, bk, hk, sk))
+
+    def terms(qh, kh, vh, gh, cols, rows):
+        logits = scale * (qh[rows] @ kh[cols].T)
+        w = np.exp(logits - logits.max(axis=-1, keepdims=True))
+        p = w / w.sum(axis=-1, keepdims=True)
+        delta = (gh[rows] * (p @ vh[cols])).sum(axis=-1)
+        return p, delta
+
+    heads = sorted(set(zip(bq.tolist(), hq.tolist())) | set(zip(bk.tolist(), hk.tolist())))
+    for (b, h) in heads:
+        qh, kh, vh, gh = (as_f64(x[b, h]) for x in (q, k, v, dout))
+        mh = head_mask(mask, h)
+        for n in np.nonzero((bq == b) & (hq == h))[0]:
+            s = int(sq[n])
+            cols = key_tokens(mh, None if s < P else (s - P) // T, T, P)
+            p, delta = terms(qh, kh, vh, gh, cols, np.array([s]))
+            ds = p * (gh[[s]] @ vh[cols].T - delta[:, None])
+            dq[n] = scale * (ds @ kh[cols])[0]
+        sel = np.nonzero((bk == b) & (hk == h))[0]
+        if sel.size == 0:
+            continue
+        keys = sk[sel]
+        for i, rows_all in _query_groups(F, T, P):
+            cols = key_tokens(mh, i, T, P)
+            hit = np.isin(keys, cols)
+            if not hit.any():
+                continue
+            tsel, kidx = sel[hit], keys[hit]
+            pos = {int(c): m for m, c in enumerate(cols)}
+            at = np.array([pos[int(t)] for t in kidx])
+            for r0 in range(0, len(rows_all), chunk):
+                rows = rows_all[r0:r0 + chunk]
+                p, delta = terms(qh, kh, vh, gh, cols, rows)
+                p_t = p[:, at]
+                ds_t = p_t * (gh[rows] @ vh[kidx].T - delta[:, None])
+                dk[tsel] += scale * (ds_t.T @ qh[rows])
+                dv[tsel] += p_t.T @ gh[rows]
+    return dq, dk, dv

@@ -419,3 +419,50 @@ def pin_mmdit_lse(lse_fn):
         logits = 0.8 * torch.from_numpy(q[:, h]) @ torch.from_numpy(k[:, h]).transpose(-1, -2)
         ref = torch.logsumexp(logits.masked_fill(~tok, float("-inf")), dim=-1).numpy()
         assert np.max(np.abs(got[:, h] - ref)) < TOL
+
+
+def pin_mmdit_bwd_matches_autograd(bwd):
+    """fn(q, k, v, dout, mask, T, P, scale) -> (dq, dk, dv) against torch autograd through
+    SDPA with the MM-DiT token mask (float64), per-head masks."""
+    rng = np.random.default_rng(40)
+    for (B, H, F, T, P, d) in [(1, 2, 3, 4, 5, 8), (2, 2, 4, 3, 1, 4), (1, 3, 3, 2, 6, 6)]:
+        q, k, v, g = (_rand(rng, B, H, P + F * T, d) for _ in range(4))
+        masks = (rng.random((H, F, F)) < 0.4).astype(np.uint8)
+        masks[0, 1, :] = 0
+        got = bwd(q, k, v, g, masks, T, P, 0.6)
+        for h in range(H):
+            tok = torch.from_numpy(_mmdit_token_mask(masks[h], F, T, P))
+            qt, kt, vt = (torch.tensor(x[:, h], requires_grad=True) for x in (q, k, v))
+            out = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=tok, scale=0.6)
+            out.backward(torch.from_numpy(g[:, h].copy()))
+            for a, t in zip(got, (qt, kt, vt)):
+                assert np.max(np.abs(a[:, h] - t.grad.numpy())) < 1e-11
+
+
+def pin_mmdit_bwd_bruteforce(bwd):
+    rng = np.random.default_rng(41)
+    F, T, P, d, scale = 2, 2, 2, 3, 0.7
+    mask = np.array([[0, 1], [0, 0]], np.uint8)
+    q, k, v, g = (_rand(rng, 1, 1, P + F * T, d, 0.8) for _ in range(4))
+    dq, dk, dv = bwd(q, k, v, g, mask, T, P, scale)
+    S = P + F * T
+    edq, edk, edv = np.zeros((S, d)), np.zeros((S, d)), np.zeros((S, d))
+    for s in range(S):
+        keys = list(range(S)) if s < P else [t for t in range(S) if t < P or mask[(s - P) // T][(t - P) // T]]
+        w = {t: math.exp(scale * sum(q[0, 0, s, c] * k[0, 0, t, c] for c in range(d))) for t in keys}
+        z = sum(w.values())
+        p = {t: w[t] / z for t in keys}
+        out = [sum(p[t] * v[0, 0, t, c] for t in keys) for c in range(d)]
+        dp = {t: sum(g[0, 0, s, c] * v[0, 0, t, c] for c in range(d)) for t in keys}
+        delta = sum(g[0, 0, s, c] * out[c] for c in range(d))
+        for t in keys:
+            ds = p[t] * (dp[t] - delta)
+            for c in range(d):
+                edq[s, c] += scale * ds * k[0, 0, t, c]
+                edk[t, c] += scale * ds * q[0, 0, s, c]
+                edv[t, c] += p[t] * g[0, 0, s, c]
+    for a, e in ((dq, edq), (dk, edk), (dv, edv)):
+        assert np.max(np.abs(a[0, 0] - e)) < TOL
+
+
+MMDIT_BWD_PINS = [pin_mmdit_bwd_matches_autograd, pin_mmdit_bwd_bruteforce]

@@ -71,3 +71,52 @@ def test_mmdit_pins_catch_planted_mistake(name, old, new):
         except Exception:
             failures += 1
     assert failures > 0, f"no pin caught: {name}"
+
+
+@pytest.mark.parametrize("pin", oracle_pins.MMDIT_BWD_PINS, ids=lambda f: f.__name__)
+def test_mmdit_bwd_pin(pin):
+    pin(om.attention_backward_mmdit)
+
+
+def test_mmdit_bwd_without_text_is_the_plain_form():
+    from oracle import backward as ob
+    rng = np.random.default_rng(42)
+    B, H, F, T, d = 1, 2, 3, 4, 5
+    q, k, v, g = (rng.standard_normal((B, H, F * T, d)) for _ in range(4))
+    masks = (rng.random((H, F, F)) < 0.5).astype(np.uint8)
+    for a, b in zip(om.attention_backward_mmdit(q, k, v, g, masks, T, 0, 0.5),
+                    ob.attention_backward(q, k, v, g, masks, T, 0.5)):
+        assert np.max(np.abs(a - b)) < 1e-12
+
+
+def test_mmdit_bwd_rows_variant_matches():
+    rng = np.random.default_rng(43)
+    B, H, F, T, P, d = 1, 2, 3, 4, 5, 6
+    q, k, v, g = (rng.standard_normal((B, H, P + F * T, d)) for _ in range(4))
+    masks = (rng.random((H, F, F)) < 0.5).astype(np.uint8)
+    masks[1, :, 0] = 0
+    full = om.attention_backward_mmdit(q, k, v, g, masks, T, P, 0.45)
+    bb, hh, ss = (x.ravel() for x in np.meshgrid(np.arange(B), np.arange(H), np.arange(P + F * T), indexing="ij"))
+    rows = om.attention_backward_mmdit_rows(q, k, v, g, masks, T, P, 0.45, bb, hh, ss, bb, hh, ss, chunk=3)
+    for a, r in zip(rows, full):
+        assert np.max(np.abs(a - r[bb, hh, ss])) < 1e-12
+
+
+BWD_MUTANTS = [
+    ("text keys get no dk", "                dk[b, h, cols] += scale * (ds.T @ qh[rows])",
+     "                dk[b, h, cols[cols >= P]] += scale * (ds.T @ qh[rows])[cols >= P]"),
+    ("delta without the text", "                ds = p * (gh[rows] @ vh[cols].T - (gh[rows] * out).sum(axis=-1, keepdims=True))",
+     "                ds = p * (gh[rows] @ vh[cols].T - (gh[rows] * (p[:, P:] @ vh[cols][P:])).sum(axis=-1, keepdims=True))"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", BWD_MUTANTS, ids=[m[0] for m in BWD_MUTANTS])
+def test_mmdit_bwd_pins_catch_planted_mistake(name, old, new):
+    mutant = _load_mutant(old, new)
+    failures = 0
+    for pin in oracle_pins.MMDIT_BWD_PINS:
+        try:
+            pin(mutant.attention_backward_mmdit)
+        except Exception:
+            failures += 1
+    assert failures > 0, f"no pin caught: {name}"
