@@ -149,12 +149,18 @@ def cpu_baseline_bwd(w, qb, kb, vb, gb, mask, budget_s: float):
         threads = os.cpu_count() or 1
     nnz = int(np.count_nonzero(mask))
     done, t0 = 0, time.perf_counter()
+    from oracle import mmdit as ommd
+
     while done < w.H and time.perf_counter() - t0 < budget_s:
         sl = slice(done, done + 1)
-        ob.attention_backward(qb[:, sl], kb[:, sl], vb[:, sl], gb[:, sl], mask, w.T, w.scale())
+        if w.prefix:
+            ommd.attention_backward_mmdit(qb[:, sl], kb[:, sl], vb[:, sl], gb[:, sl], mask, w.T, w.prefix,
+                                          w.scale())
+        else:
+            ob.attention_backward(qb[:, sl], kb[:, sl], vb[:, sl], gb[:, sl], mask, w.T, w.scale())
         done += 1
     dt = time.perf_counter() - t0
-    flop = 10.0 * w.B * done * w.d * float(w.T) ** 2 * nnz
+    flop = kept_flop(w, nnz, "bwd") * done / w.H
     return {
         "value": flop / dt / 1e12,
         "unit": "TFLOP/s",
@@ -169,7 +175,7 @@ def make_grad_bits(w, seed: int = 1):
     """Upstream gradient dO: N(0, 1) per element as bf16 bits, one PCG64 stream."""
     rng = np.random.default_rng(seed)
     return workloads.f32_to_bf16_bits(
-        rng.standard_normal((w.B, w.H, w.F * w.T, w.d), dtype=np.float32))
+        rng.standard_normal((w.B, w.H, w.S, w.d), dtype=np.float32))
 
 
 class Problem:
@@ -198,11 +204,14 @@ class Problem:
                                                   w.scale(), None, st)
         if self.which == "fwd":
             return lambda: ta.tile_attn_fwd(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), st)
-        if w.prefix:
-            raise SystemExit("the gradients of the MM-DiT form are not implemented")
         # out and lse of this mask, once, outside the timed region
-        ta.tile_attn_fwd_heads(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), self.lse, st)
         dq, dk, dv = self.grads
+        if w.prefix:
+            ta.tile_attn_fwd_mmdit(q, k, v, out, w.B, w.H, w.F, w.T, w.prefix, w.d, mask, w.scale(),
+                                   self.lse, st)
+            return lambda: ta.tile_attn_bwd_mmdit(q, k, v, out, self.dout, self.lse, dq, dk, dv, w.B,
+                                                  w.H, w.F, w.T, w.prefix, w.d, mask, w.scale(), st)
+        ta.tile_attn_fwd_heads(q, k, v, out, w.B, w.H, w.F, w.T, w.d, mask, w.scale(), self.lse, st)
         return lambda: ta.tile_attn_bwd(q, k, v, out, self.dout, self.lse, dq, dk, dv, w.B, w.H, w.F,
                                         w.T, w.d, mask, w.scale(), st)
 

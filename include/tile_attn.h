@@ -155,6 +155,21 @@ int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out,
                   const uint8_t* tile_masks, int n_masks, float scale, void* stream);
 
 /*
+ * Gradients of the MM-DiT form (tile_attn_fwd_mmdit): the same chain rule over the
+ * query-key pairs that form keeps (text rows and text columns dense, the video masks
+ * on the video-video part), for training a sparse MM-DiT student (App. E applies
+ * the method's distillation to CogVideoX). Tensors are [B, H, P + F*T, d] with the
+ * P text tokens first; out and lse come from tile_attn_fwd_mmdit with the same
+ * masks and scale. P = 0 is tile_attn_bwd. Every key is kept by the text queries,
+ * so the key side plans the transposed (F+1) x (F+1) mask, whose text row is
+ * split. Errors: those of tile_attn_bwd; TA_ERR_BAD_SHAPE also for P < 0.
+ */
+int tile_attn_bwd_mmdit(const void* q, const void* k, const void* v, const void* out,
+                        const void* dout, const float* lse, void* dq, void* dk, void* dv,
+                        int B, int H, int F, int T, int P, int d,
+                        const uint8_t* tile_masks, int n_masks, float scale, void* stream);
+
+/*
  * Dense control: 3D full attention (every tile kept, the "full" rows of
  * tab:kernel_time). Runs the same kernel as tile_attn_fwd with an all-ones
  * mask, so its output is bit-identical to tile_attn_fwd with that mask.

@@ -13,6 +13,7 @@ from .api import (  # noqa: F401
     dense_attn_fwd,
     tile_attn,
     tile_attn_bwd,
+    tile_attn_bwd_mmdit,
     tile_attn_compact,
     tile_attn_fwd,
     tile_attn_fwd_heads,

@@ -15,6 +15,7 @@ EXPORTS = (
     "tile_attn_fwd_heads",
     "tile_attn_fwd_mmdit",
     "tile_attn_bwd",
+    "tile_attn_bwd_mmdit",
     "dense_attn_fwd",
     "tile_attn_make_mask",
     "tile_attn_compact",
@@ -57,6 +58,8 @@ def _load() -> ctypes.CDLL:
     lib.tile_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, vp, ci,
                                   cf, vp]
     lib.tile_attn_bwd.restype = ci
+    lib.tile_attn_bwd_mmdit.argtypes = [vp] * 9 + [ci] * 6 + [vp, ci, cf, vp]
+    lib.tile_attn_bwd_mmdit.restype = ci
     lib.dense_attn_fwd.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, cf, vp]
     lib.dense_attn_fwd.restype = ci
     lib.tile_attn_make_mask.argtypes = [ci, ci, ci, vp]

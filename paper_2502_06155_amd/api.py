@@ -101,6 +101,19 @@ def tile_attn_bwd(q, k, v, out, dout, lse, dq, dk, dv, B: int, H: int, F: int, T
                              n_masks, float(scale), _stream(stream)), "tile_attn_bwd")
 
 
+def tile_attn_bwd_mmdit(q, k, v, out, dout, lse, dq, dk, dv, B: int, H: int, F: int, T: int,
+                        P: int, d: int, tile_masks, scale: float, stream=None) -> None:
+    """tile_attn_bwd_mmdit of the C ABI: gradients of the MM-DiT form ([B, H, P + F*T, d],
+    text first) from tile_attn_fwd_mmdit's out and lse."""
+    m = np.ascontiguousarray(np.asarray(tile_masks), dtype=np.uint8)
+    if m.size % (F * F):
+        raise ValueError("tile_masks must hold n_masks * F * F entries")
+    n_masks = m.size // (F * F)
+    _check(lib.tile_attn_bwd_mmdit(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+                                   _ptr(dq), _ptr(dk), _ptr(dv), B, H, F, T, P, d, m.ctypes.data,
+                                   n_masks, float(scale), _stream(stream)), "tile_attn_bwd_mmdit")
+
+
 def dense_attn_fwd(q, k, v, out, B: int, H: int, F: int, T: int, d: int, scale: float,
                    stream=None) -> None:
     """dense_attn_fwd of the C ABI: every tile kept."""

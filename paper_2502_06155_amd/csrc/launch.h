@@ -79,6 +79,7 @@ struct BwdArgs {
   uint16_t* dk;
   uint16_t* dv;
   int B, H, F, T, d;
+  int P;  // text tokens before the video (0: none); segments as in FwdArgs
   const float* lse2;
   const float* delta;
   const int32_t* items_q;
@@ -94,16 +95,17 @@ struct BwdArgs {
   float scale;       // multiplies dq and dk
   uint32_t flip;     // 0x80008000 flips the sign of the logits' q (dq pass) or k (dk/dv pass)
   uint32_t keep;     // 0 zeroes that operand (scale 0), else ~0
-  uint32_t n_wg_q;   // B * n_items_q * ceil(T / bwd_queries_per_workgroup(d))
-  uint32_t n_wg_k;   // B * n_items_k * ceil(T / bwd_keys_per_workgroup(d))
+  uint32_t n_wg_q;   // B * n_items_q * ceil(max(T, P) / bwd_queries_per_workgroup(d))
+  uint32_t n_wg_k;   // B * n_items_k * ceil(max(T, P) / bwd_keys_per_workgroup(d))
 };
 
-// Adds the partials of split frames: heavy holds {head, frame, first slot, slots}.
+// Adds the partials of split segments: heavy holds {head, segment, first slot, slots}.
 struct SumArgs {
   const float* ws;
   const int32_t* heavy;
   int n_heavy;
   int B, H, F, T, d;
+  int P;
   uint16_t* out;
 };
 

@@ -41,6 +41,8 @@
 #include <float.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "launch.h"
 #include "tile_common.h"
 
@@ -262,7 +264,7 @@ __device__ __forceinline__ void dq_scores(const f32x16& s, const f32x16& dp, flo
   }
 }
 
-template <int D>
+template <int D, bool PREFIX>
 __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a, int nqb) {
   using Sh = BShape<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
@@ -277,21 +279,25 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
   const int frame = item[1], kbeg = item[2], n_kept = item[3], slot = item[4];
   const int qb = (int)(rem % nqb);
   const int T = a.T;
+  const Layout<PREFIX> lay{a.F, T, a.P};
+  const int seg0 = lay.start(frame), seg_len = lay.len(frame);
+  // With a prefix the text segment is shorter than the grid's query blocks assume.
+  if (PREFIX && qb * kRowsPerWg >= seg_len) return;
 
-  const size_t head_elems = (size_t)a.F * T * D;
-  const uint16_t* Kh = a.k + bh * head_elems;
-  const uint16_t* Vh = a.v + bh * head_elems;
+  const size_t head_rows = (size_t)a.P * PREFIX + (size_t)a.F * T;
+  const uint16_t* Kh = a.k + bh * head_rows * D;
+  const uint16_t* Vh = a.v + bh * head_rows * D;
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hf = lane >> 5;
   const int qrow = qb * kRowsPerWg + wave * 32 + n;
-  const bool wave_active = qb * kRowsPerWg + wave * 32 < T;
+  const bool wave_active = qb * kRowsPerWg + wave * 32 < seg_len;
 
   // This lane's query: Q^T and dO^T B-operand slices, its lse (base 2) and delta.
   bf16x8 qf[Sh::kChunks], gf[Sh::kChunks];
-  const bool valid = qrow < T;
-  const size_t qr = ((size_t)bh * a.F + frame) * T + qrow;
+  const bool valid = qrow < seg_len;
+  const size_t qr = (size_t)bh * head_rows + seg0 + qrow;
   load_row_operand<D>(a.q + qr * D, valid, a.keep, a.flip, hf, qf);
   load_row_operand<D>(a.dout + qr * D, valid, ~0u, 0u, hf, gf);
   const float lse2 = valid ? a.lse2[qr] : 0.f;
@@ -302,7 +308,11 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
   for (int mb = 0; mb < Sh::kDBlocks; ++mb) acc[mb] = f32x16{};
 
   const int tpf = (T + kBlockK - 1) / kBlockK;
-  const int n_tiles = n_kept * tpf;
+  int n_tiles = n_kept * tpf;
+  if constexpr (PREFIX) {
+    // the text segment (index F) sorts last in a kept list
+    if (n_kept > 0 && a.cols_q[kbeg + n_kept - 1] == a.F) n_tiles += (a.P + kBlockK - 1) / kBlockK - tpf;
+  }
   if (n_tiles > 0) {
     DualLoader<D> ld;
     ld.init(wave, lane);
@@ -310,8 +320,8 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
     ra.init(n, hf);
     TrAddr<D> ta;
     ta.init(lane);
-    TileCursor cur, nxt;
-    cur.start(a.cols_q + kbeg, tpf, T);
+    SegmentCursor<PREFIX> cur, nxt;
+    cur.start(a.cols_q + kbeg, lay);
     ld.load(Kh, cur.key0(), cur.nvalid(), sK[0], wave);
     ld.load(Vh, cur.key0(), cur.nvalid(), sV[0], wave);
     nxt = cur;
@@ -369,11 +379,12 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
     }
   }
 
-  if (qrow < T) {
+  if (qrow < seg_len) {
     if (slot < 0) {
       store_row_bf16<D>(a.dq + qr * D, acc, a.scale, hf);
     } else {
-      const size_t prow = ((size_t)slot * a.B + b) * T + qrow;
+      const int slot_rows = PREFIX ? max(T, a.P) : T;
+      const size_t prow = ((size_t)slot * a.B + b) * slot_rows + qrow;
       store_row_f32<D>(a.ws_dq + prow * D, acc, a.scale, hf);
     }
   }
@@ -381,7 +392,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
 
 // ---------------------------------------------------------------------------
 // dk/dv pass.
-template <int D>
+template <int D, bool PREFIX>
 __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_kernel(const BwdArgs a,
                                                                                      int nkb) {
   using Sh = BShape<D>;
@@ -399,8 +410,11 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   const int frame = item[1], qbeg = item[2], n_keep = item[3], slot = item[4];
   const int kblk = (int)(rem % nkb);
   const int T = a.T;
+  const Layout<PREFIX> lay{a.F, T, a.P};
+  const int seg0 = lay.start(frame), seg_len = lay.len(frame);
+  if (PREFIX && kblk * kRowsPerWg >= seg_len) return;
 
-  const size_t head_rows = (size_t)a.F * T;
+  const size_t head_rows = (size_t)a.P * PREFIX + (size_t)a.F * T;
   const uint16_t* Qh = a.q + bh * head_rows * D;
   const uint16_t* Gh = a.dout + bh * head_rows * D;
   const float* Lh = a.lse2 + bh * head_rows;
@@ -410,12 +424,12 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 31, hf = lane >> 5;
   const int krow = kblk * kRowsPerWg + wave * 32 + n;
-  const bool wave_active = kblk * kRowsPerWg + wave * 32 < T;
+  const bool wave_active = kblk * kRowsPerWg + wave * 32 < seg_len;
 
   // This lane's key as B operand of S = Q K^T and dP = dO V^T.
   bf16x8 kf[Sh::kChunks], vf[Sh::kChunks];
-  const bool valid = krow < T;
-  const size_t kr = ((size_t)bh * a.F + frame) * T + krow;
+  const bool valid = krow < seg_len;
+  const size_t kr = (size_t)bh * head_rows + seg0 + krow;
   load_row_operand<D>(a.k + kr * D, valid, a.keep, a.flip, hf, kf);
   load_row_operand<D>(a.v + kr * D, valid, ~0u, 0u, hf, vf);
 
@@ -427,7 +441,10 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   }
 
   const int tpf = (T + kBlockK - 1) / kBlockK;
-  const int n_tiles = n_keep * tpf;
+  int n_tiles = n_keep * tpf;
+  if constexpr (PREFIX) {
+    if (n_keep > 0 && a.cols_k[qbeg + n_keep - 1] == a.F) n_tiles += (a.P + kBlockK - 1) / kBlockK - tpf;
+  }
   if (n_tiles > 0) {
     DualLoader<D> ld;
     ld.init(wave, lane);
@@ -437,7 +454,7 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
     ta.init(lane);
     // Q, dO, lse2 and delta of one 64-query tile; rows past the valid range read
     // as zeros, so they add exactly nothing below (zero Q and dO rows, P <= 1).
-    auto load_tile = [&](const TileCursor& tc, int bi) {
+    auto load_tile = [&](const SegmentCursor<PREFIX>& tc, int bi) {
       const size_t row0 = tc.key0();
       const int nv = tc.nvalid();
       ld.load(Qh, row0, nv, sQ[bi], wave);
@@ -449,8 +466,8 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
                           4 * lane);
       }
     };
-    TileCursor cur, nxt;
-    cur.start(a.cols_k + qbeg, tpf, T);
+    SegmentCursor<PREFIX> cur, nxt;
+    cur.start(a.cols_k + qbeg, lay);
     load_tile(cur, 0);
     nxt = cur;
     nxt.advance(n_keep);
@@ -525,12 +542,13 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   }
 
   // dK uses the unflipped q of the LDS tiles, so scale (with its sign) applies.
-  if (krow < T) {
+  if (krow < seg_len) {
     if (slot < 0) {
       store_row_bf16<D>(a.dk + kr * D, dk, a.scale, hf);
       store_row_bf16<D>(a.dv + kr * D, dv, 1.f, hf);
     } else {
-      const size_t prow = ((size_t)slot * a.B + b) * T + krow;
+      const int slot_rows = PREFIX ? max(T, a.P) : T;
+      const size_t prow = ((size_t)slot * a.B + b) * slot_rows + krow;
       store_row_f32<D>(a.ws_dk + prow * D, dk, a.scale, hf);
       store_row_f32<D>(a.ws_dv + prow * D, dv, 1.f, hf);
     }
@@ -538,24 +556,29 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
 }
 
 // ---------------------------------------------------------------------------
-// Sum of the partials of split frames: one thread per (split frame, batch entry,
-// row, 8 consecutive d), rounded to bf16 (RNE).
+// Sum of the partials of split segments: one thread per (split segment, batch
+// entry, row, 8 consecutive d), rounded to bf16 (RNE). Partials are laid out
+// [slot][batch][L][d] with L = max(T, P) rows per slot (T without a prefix).
 template <int D>
 __global__ __launch_bounds__(256) void sum_partials_kernel(const float* __restrict__ ws,
                                                            const int32_t* __restrict__ heavy,
                                                            int n_heavy, int B, int H, int F, int T,
-                                                           uint16_t* __restrict__ out) {
+                                                           int P, uint16_t* __restrict__ out) {
   constexpr int kGroups = D / 8;
+  const int L = max(T, P);
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t per_frame = (size_t)B * T * kGroups;
-  if (idx >= per_frame * (size_t)n_heavy) return;
-  const int hv = (int)(idx / per_frame);
-  const size_t r = idx - (size_t)hv * per_frame;
+  const size_t per_seg = (size_t)B * L * kGroups;
+  if (idx >= per_seg * (size_t)n_heavy) return;
+  const int hv = (int)(idx / per_seg);
+  const size_t r = idx - (size_t)hv * per_seg;
   const int grp = (int)(r % kGroups);
-  const size_t row = r / kGroups;  // b * T + t
+  const size_t row = r / kGroups;  // b * L + t
+  const size_t b = row / L, t = row - b * L;
   const int head = heavy[4 * hv], frame = heavy[4 * hv + 1];
   const int slot0 = heavy[4 * hv + 2], np = heavy[4 * hv + 3];
-  const size_t slot_stride = (size_t)B * T;
+  const int seg0 = frame < F ? P + frame * T : 0, seg_len = frame < F ? T : P;
+  if ((int)t >= seg_len) return;
+  const size_t slot_stride = (size_t)B * L;
   f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
   for (int p = 0; p < np; ++p) {
     const f32x4* src =
@@ -563,8 +586,7 @@ __global__ __launch_bounds__(256) void sum_partials_kernel(const float* __restri
     a0 += src[0];
     a1 += src[1];
   }
-  const size_t b = row / T, t = row - b * T;
-  const size_t orow = ((b * H + head) * F + frame) * (size_t)T + t;
+  const size_t orow = (b * H + head) * ((size_t)P + (size_t)F * T) + seg0 + t;
   const f32x8 x = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
   *reinterpret_cast<bf16x8*>(out + orow * D + 8 * grp) = __builtin_convertvector(x, bf16x8);
 }
@@ -579,24 +601,30 @@ hipError_t prep_d(const PrepArgs& a, hipStream_t stream) {
 
 template <int D>
 hipError_t dq_d(const BwdArgs& a, hipStream_t stream) {
-  const int nqb = (a.T + kRowsPerWg - 1) / kRowsPerWg;
-  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(a.n_wg_q), dim3(kBwdThreads), 0, stream, a, nqb);
+  const int nqb = (std::max(a.T, a.P) + kRowsPerWg - 1) / kRowsPerWg;
+  if (a.P > 0)
+    hipLaunchKernelGGL((bwd_dq_kernel<D, true>), dim3(a.n_wg_q), dim3(kBwdThreads), 0, stream, a, nqb);
+  else
+    hipLaunchKernelGGL((bwd_dq_kernel<D, false>), dim3(a.n_wg_q), dim3(kBwdThreads), 0, stream, a, nqb);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t dkdv_d(const BwdArgs& a, hipStream_t stream) {
-  const int nkb = (a.T + kRowsPerWg - 1) / kRowsPerWg;
-  hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream, a, nkb);
+  const int nkb = (std::max(a.T, a.P) + kRowsPerWg - 1) / kRowsPerWg;
+  if (a.P > 0)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream, a, nkb);
+  else
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream, a, nkb);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t sum_d(const SumArgs& a, hipStream_t stream) {
-  const size_t threads = (size_t)a.n_heavy * a.B * a.T * (D / 8);
+  const size_t threads = (size_t)a.n_heavy * a.B * std::max(a.T, a.P) * (D / 8);
   const size_t blocks = (threads + 255) / 256;
   hipLaunchKernelGGL(sum_partials_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.ws,
-                     a.heavy, a.n_heavy, a.B, a.H, a.F, a.T, a.out);
+                     a.heavy, a.n_heavy, a.B, a.H, a.F, a.T, a.P, a.out);
   return hipGetLastError();
 }
 

@@ -331,38 +331,51 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
 // each), then the dq partials and the dk, dv partials.
 int run_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
             const float* lse, void* dq, void* dk, void* dv, int B, int H, int F, int T, int d,
-            const uint8_t* masks, int n_masks, float scale, void* stream) {
+            const uint8_t* masks, int n_masks, float scale, void* stream, int P = 0) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
   const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
+  const int L = std::max(T, P);  // longest segment
   const int qpw = ta::bwd_queries_per_workgroup(d);
-  const int64_t nqb = (T + qpw - 1) / qpw;
+  const int64_t nqb = (L + qpw - 1) / qpw;
   const int kpw = ta::bwd_keys_per_workgroup(d);
-  const int64_t nkb = (T + kpw - 1) / kpw;
-  const size_t part_row = (size_t)B * T * d * sizeof(float);
+  const int64_t nkb = (L + kpw - 1) / kpw;
+  const size_t part_row = (size_t)B * L * d * sizeof(float);
 
+  // Segments: the F frames, plus the text (segment F) with a prefix, whose row and
+  // column the (F+1) x (F+1) mask keeps entirely.
+  const int n_seg = P > 0 ? F + 1 : F;
+  std::vector<uint8_t> aug;
+  if (P > 0) {
+    aug.assign((size_t)n_masks * n_seg * n_seg, 1);
+    for (int m = 0; m < n_masks; ++m)
+      for (int i = 0; i < F; ++i)
+        for (int j = 0; j < F; ++j)
+          aug[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * F + i) * F + j] ? 1 : 0;
+    masks = aug.data();
+  }
   const DeviceWorkList* wq = nullptr;
-  int st = work_list_for(masks, n_masks, H, F, true, dev, &wq);
+  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &wq);
   if (st != TA_OK) return st;
   if ((size_t)wq->n_slots * part_row > kMaxWorkspaceBytes || (int64_t)B * wq->n_items * nqb > max_wg) {
-    st = work_list_for(masks, n_masks, H, F, false, dev, &wq);
+    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &wq);
     if (st != TA_OK) return st;
   }
-  std::vector<uint8_t> mt((size_t)n_masks * F * F);
+  std::vector<uint8_t> mt((size_t)n_masks * n_seg * n_seg);
   for (int m = 0; m < n_masks; ++m)
-    for (int i = 0; i < F; ++i)
-      for (int j = 0; j < F; ++j)
-        mt[((size_t)m * F + i) * F + j] = masks[((size_t)m * F + j) * F + i];
+    for (int i = 0; i < n_seg; ++i)
+      for (int j = 0; j < n_seg; ++j)
+        mt[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * n_seg + j) * n_seg + i];
   const DeviceWorkList* wk = nullptr;
-  st = work_list_for(mt.data(), n_masks, H, F, true, dev, &wk);
+  st = work_list_for(mt.data(), n_masks, H, n_seg, true, dev, &wk);
   if (st != TA_OK) return st;
   if ((size_t)wk->n_slots * 2 * part_row > kMaxWorkspaceBytes || (int64_t)B * wk->n_items * nkb > max_wg) {
-    st = work_list_for(mt.data(), n_masks, H, F, false, dev, &wk);
+    st = work_list_for(mt.data(), n_masks, H, n_seg, false, dev, &wk);
     if (st != TA_OK) return st;
   }
 
-  const size_t rows = (size_t)B * H * F * T;
+  const size_t rows = (size_t)B * H * ((size_t)F * T + P);
   const size_t bytes = rows * 2 * sizeof(float) + (size_t)wq->n_slots * part_row +
                        (size_t)wk->n_slots * 2 * part_row;
   void* ws = nullptr;
@@ -371,8 +384,8 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
   float* lse2 = static_cast<float*>(ws);
   float* delta = lse2 + rows;
   float* ws_dq = delta + rows;
-  float* ws_dk = ws_dq + (size_t)wq->n_slots * B * T * d;
-  float* ws_dv = ws_dk + (size_t)wk->n_slots * B * T * d;
+  float* ws_dk = ws_dq + (size_t)wq->n_slots * B * L * d;
+  float* ws_dv = ws_dk + (size_t)wk->n_slots * B * L * d;
   const hipStream_t s = static_cast<hipStream_t>(stream);
 
   ta::PrepArgs pa;
@@ -399,6 +412,7 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
   a.F = F;
   a.T = T;
   a.d = d;
+  a.P = P;
   a.lse2 = lse2;
   a.delta = delta;
   a.items_q = wq->items;
@@ -439,6 +453,7 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
     m.F = F;
     m.T = T;
     m.d = d;
+    m.P = P;
     m.out = static_cast<uint16_t*>(dst);
     hipError_t err = ta::launch_sum_partials(m, s);
     if (err != hipSuccess)
@@ -551,12 +566,16 @@ int dense_attn_fwd(const void* q, const void* k, const void* v, void* out, int B
   return run_fwd(q, k, v, out, B, H, F, T, d, ones.data(), 1, scale, nullptr, stream);
 }
 
-int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
-                  const float* lse, void* dq, void* dk, void* dv, int B, int H, int F, int T, int d,
-                  const uint8_t* tile_masks, int n_masks, float scale, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int check_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
+              const float* lse, void* dq, void* dk, void* dv, int B, int H, int F, int T, int P,
+              int d, const uint8_t* tile_masks, int n_masks, float scale) {
   if (!out || !dout || !lse || !dq || !dk || !dv)
     return fail(TA_ERR_NULL_PTR, "out, dout, lse, dq, dk and dv must be non-NULL");
-  int st = check_args(q, k, v, dq, B, H, F, T, d, scale);
+  int st = check_args(q, k, v, dq, B, H, F, T, d, scale, P);
   if (st != TA_OK) return st;
   if (!tile_masks) return fail(TA_ERR_NULL_PTR, "tile_masks must be non-NULL");
   if (n_masks != 1 && n_masks != H) return fail(TA_ERR_BAD_MASK, "n_masks must be 1 or H");
@@ -565,11 +584,13 @@ int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out, 
       return fail(TA_ERR_ALIGN, "q, k, v, out, dout, dq, dk and dv must be 16-byte aligned");
   if (reinterpret_cast<uintptr_t>(lse) % 4) return fail(TA_ERR_ALIGN, "lse must be 4-byte aligned");
   const int kpw = ta::bwd_keys_per_workgroup(d), qpw = ta::bwd_queries_per_workgroup(d);
-  if ((int64_t)B * H * F * ((T + std::min(kpw, qpw) - 1) / std::min(kpw, qpw)) * ta::kThreads >
-      (int64_t)UINT32_MAX)
+  const int L = std::max(T, P);
+  if ((int64_t)B * H * (F + (P > 0)) * ((L + std::min(kpw, qpw) - 1) / std::min(kpw, qpw)) *
+          ta::kThreads > (int64_t)UINT32_MAX)
     return fail(TA_ERR_BAD_SHAPE, "the gradient passes would exceed the grid limit");
-  const size_t bytes = (size_t)B * H * F * T * d * 2;
-  const size_t lbytes = (size_t)B * H * F * T * sizeof(float);
+  const size_t rows = (size_t)B * H * ((size_t)F * T + P);
+  const size_t bytes = rows * d * 2;
+  const size_t lbytes = rows * sizeof(float);
   const void* outs[3] = {dq, dk, dv};
   for (int i = 0; i < 3; ++i) {
     for (const void* p : {q, k, v, out, dout})
@@ -581,8 +602,32 @@ int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out, 
       if (ranges_overlap(outs[i], bytes, outs[j], bytes))
         return fail(TA_ERR_OVERLAP, "dq, dk and dv must not overlap each other");
   }
+  return TA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tile_attn_bwd(const void* q, const void* k, const void* v, const void* out, const void* dout,
+                  const float* lse, void* dq, void* dk, void* dv, int B, int H, int F, int T, int d,
+                  const uint8_t* tile_masks, int n_masks, float scale, void* stream) {
+  const int st = check_bwd(q, k, v, out, dout, lse, dq, dk, dv, B, H, F, T, 0, d, tile_masks,
+                           n_masks, scale);
+  if (st != TA_OK) return st;
   return run_bwd(q, k, v, out, dout, lse, dq, dk, dv, B, H, F, T, d, tile_masks, n_masks, scale,
                  stream);
+}
+
+int tile_attn_bwd_mmdit(const void* q, const void* k, const void* v, const void* out,
+                        const void* dout, const float* lse, void* dq, void* dk, void* dv, int B,
+                        int H, int F, int T, int P, int d, const uint8_t* tile_masks, int n_masks,
+                        float scale, void* stream) {
+  const int st = check_bwd(q, k, v, out, dout, lse, dq, dk, dv, B, H, F, T, P, d, tile_masks,
+                           n_masks, scale);
+  if (st != TA_OK) return st;
+  return run_bwd(q, k, v, out, dout, lse, dq, dk, dv, B, H, F, T, d, tile_masks, n_masks, scale,
+                 stream, P);
 }
 
 const char* tile_attn_status_string(int status) {

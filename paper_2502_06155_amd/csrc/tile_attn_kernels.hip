@@ -249,52 +249,6 @@ __device__ __forceinline__ float block_weights(const f32x16& s, float c, float m
   return ls;
 }
 
-// Token layout of one (batch, head). Without a prefix: F frames of T tokens,
-// segment j = frame j at j*T. With a prefix (the MM-DiT form): P text tokens first,
-// then the frames, so segment j < F starts at P + j*T and segment F is the text,
-// P tokens at 0.
-template <bool PREFIX>
-struct Layout {
-  int F, T, P;
-  __device__ __forceinline__ int start(int j) const {
-    if constexpr (PREFIX) return j < F ? P + j * T : 0;
-    else return j * T;
-  }
-  __device__ __forceinline__ int len(int j) const {
-    if constexpr (PREFIX) return j < F ? T : P;
-    else return T;
-  }
-};
-
-// Walks the 64-token tiles of a list of segments (frames, and the text segment with
-// a prefix) in order; all state is wave-uniform. Without a prefix this is
-// TileCursor.
-template <bool PREFIX>
-struct SegmentCursor {
-  const int32_t* cols;
-  Layout<PREFIX> L;
-  int e = 0, kt = 0, kf = 0, tiles = 0;
-  __device__ __forceinline__ void start(const int32_t* c, Layout<PREFIX> lay) {
-    cols = c;
-    L = lay;
-    e = 0;
-    kt = 0;
-    kf = cols[0];
-    tiles = (L.len(kf) + kBlockK - 1) / kBlockK;
-  }
-  __device__ __forceinline__ void advance(int n_segments) {
-    if (++kt == tiles) {
-      kt = 0;
-      if (++e < n_segments) {
-        kf = cols[e];
-        tiles = (L.len(kf) + kBlockK - 1) / kBlockK;
-      }
-    }
-  }
-  __device__ __forceinline__ size_t key0() const { return (size_t)L.start(kf) + kt * kBlockK; }
-  __device__ __forceinline__ int nvalid() const { return min(kBlockK, L.len(kf) - kt * kBlockK); }
-};
-
 template <int D, bool PREFIX>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,

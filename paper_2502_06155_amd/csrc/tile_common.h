@@ -42,29 +42,51 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Walks the tiles of a list of frames in order: tile (e, kt) covers tokens
-// [64*kt, 64*kt + 64) of frame cols[e]. All state is wave-uniform (SGPRs); the
-// list is read with one scalar load per frame.
-struct TileCursor {
-  const int32_t* cols;  // the frames to walk
-  int e = 0, kt = 0, kf = 0;
-  int tiles_per_frame, T;
-  __device__ __forceinline__ void start(const int32_t* c, int tpf, int t_len) {
+// Token layout of one (batch, head). Without a prefix: F frames of T tokens,
+// segment j = frame j at j*T. With a prefix (the MM-DiT form): P text tokens first,
+// then the frames, so segment j < F starts at P + j*T and segment F is the text,
+// P tokens at 0.
+template <bool PREFIX>
+struct Layout {
+  int F, T, P;
+  __device__ __forceinline__ int start(int j) const {
+    if constexpr (PREFIX) return j < F ? P + j * T : 0;
+    else return j * T;
+  }
+  __device__ __forceinline__ int len(int j) const {
+    if constexpr (PREFIX) return j < F ? T : P;
+    else return T;
+  }
+};
+
+// Walks the 64-token tiles of a list of segments (frames, and the text segment with
+// a prefix) in order: tile (e, kt) covers tokens [64 kt, 64 kt + 64) of segment
+// cols[e]. All state is wave-uniform (SGPRs); the list is read with one scalar load
+// per segment.
+template <bool PREFIX>
+struct SegmentCursor {
+  const int32_t* cols;
+  Layout<PREFIX> L;
+  int e = 0, kt = 0, kf = 0, tiles = 0;
+  __device__ __forceinline__ void start(const int32_t* c, Layout<PREFIX> lay) {
     cols = c;
-    tiles_per_frame = tpf;
-    T = t_len;
+    L = lay;
     e = 0;
     kt = 0;
     kf = cols[0];
+    tiles = (L.len(kf) + kBlockK - 1) / kBlockK;
   }
-  __device__ __forceinline__ void advance(int n_frames) {
-    if (++kt == tiles_per_frame) {
+  __device__ __forceinline__ void advance(int n_segments) {
+    if (++kt == tiles) {
       kt = 0;
-      if (++e < n_frames) kf = cols[e];
+      if (++e < n_segments) {
+        kf = cols[e];
+        tiles = (L.len(kf) + kBlockK - 1) / kBlockK;
+      }
     }
   }
-  __device__ __forceinline__ size_t key0() const { return (size_t)kf * T + kt * kBlockK; }
-  __device__ __forceinline__ int nvalid() const { return min(kBlockK, T - kt * kBlockK); }
+  __device__ __forceinline__ size_t key0() const { return (size_t)L.start(kf) + kt * kBlockK; }
+  __device__ __forceinline__ int nvalid() const { return min(kBlockK, L.len(kf) - kt * kBlockK); }
 };
 
 // Both halves of the wave see max/sum over lanes l and l^32 (v_permlane32_swap
@@ -81,10 +103,14 @@ __device__ __forceinline__ float pair_sum(float x) {
 }
 
 // Buffer resource words (raw buffer, no stride) over `bytes` bytes at `base`;
-// loads past the end return zero, which keeps tile loads inside their frame.
+// loads past the end return zero, which keeps tile loads inside their frame. The
+// base and size are wave-uniform (one tile per workgroup); readfirstlane states so,
+// which keeps the descriptor in SGPRs even where the compiler cannot prove it.
 __device__ __forceinline__ i32x4 buffer_words(const void* base, uint32_t bytes) {
   const uint64_t a = reinterpret_cast<uint64_t>(base);
-  return i32x4{(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xffffu), (int)bytes, 0x00020000};
+  return i32x4{__builtin_amdgcn_readfirstlane((int)(uint32_t)a),
+               __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu)),
+               __builtin_amdgcn_readfirstlane((int)bytes), 0x00020000};
 }
 
 // One 16-byte-per-lane buffer load written straight to LDS: lane L's 16 bytes

@@ -222,3 +222,20 @@ def test_mmdit_argument_errors_before_any_gpu_call():
     assert _mmdit(lse=(1 << 20) | 2) == 5
     assert _mmdit(lse=(2 << 13) + 5000) == 7  # lse overlaps k's last rows
     assert _mmdit(T=2 ** 30, F=2, P=2 ** 30) == 2  # P + F*T overflows
+
+
+def test_bwd_mmdit_argument_errors_before_any_gpu_call():
+    # B=1, H=2, F=2, T=8, P=5, d=64: 21 tokens, 5376 bytes per tensor; pointers 8 KiB apart
+    base = dict(q=1 << 13, k=2 << 13, v=3 << 13, out=4 << 13, dout=5 << 13, lse=6 << 13, dq=7 << 13,
+                dk=8 << 13, dv=9 << 13)
+
+    def call(P=5, d=64, n=2, **kw):
+        a = dict(base, **kw)
+        m = np.ones((2, 2, 2), np.uint8)
+        return lib.tile_attn_bwd_mmdit(a["q"], a["k"], a["v"], a["out"], a["dout"], a["lse"], a["dq"],
+                                       a["dk"], a["dv"], 1, 2, 2, 8, P, d, m.ctypes.data, n, 0.1, None)
+
+    assert call(P=-1) == 2 and call(d=80) == 3 and call(n=3) == 4
+    assert call(dout=None) == 1
+    assert call(dq=(1 << 13) + 4096) == 7  # dq overlaps q over P + F*T tokens
+    assert call(dk=(9 << 13) - 4096) == 7  # dk overlaps dv

@@ -11,6 +11,7 @@ import pytest
 import workloads
 from oracle import backward as ob
 from oracle import masks as om
+from oracle import mmdit as ommd
 from tests.gpu_helpers import from_dev, to_dev, widen
 
 pytestmark = pytest.mark.gpu
@@ -247,3 +248,71 @@ def test_bwd_full_size_sampled(name, form, g):
     assert_grad(dv[bk, hk, sk], rv, f"{name}-{form}-dv")
     for x in (dq, dk, dv):
         assert np.all(np.isfinite(widen(x[:, :, :: max(1, w.T // 7)])))
+
+
+# ---- the MM-DiT form (text prefix) ------------------------------------------------------
+
+def run_gpu_bwd_mmdit(qb, kb, vb, gb, masks, T, P, scale):
+    B, H, S, d = qb.shape
+    F = (S - P) // T
+    q, k, v, g = (to_dev(x) for x in (qb, kb, vb, gb))
+    out = torch.empty_like(q)
+    lse = torch.empty((B, H, S), dtype=torch.float32, device="cuda")
+    grads = [torch.full_like(q, float("nan")) for _ in range(3)]
+    s = torch.cuda.current_stream()
+    ta.tile_attn_fwd_mmdit(q, k, v, out, B, H, F, T, P, d, masks, scale, lse, s)
+    ta.tile_attn_bwd_mmdit(q, k, v, out, g, lse, *grads, B, H, F, T, P, d, masks, scale, s)
+    torch.cuda.synchronize()
+    return tuple(from_dev(x) for x in grads)
+
+
+@pytest.mark.parametrize("d", [64, 96, 128])
+@pytest.mark.parametrize("T,P", [(130, 17), (64, 226), (65, 1), (40, 300)])
+def test_bwd_mmdit_small(d, T, P):
+    B, H, F = 2, 2, 4
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=T + P + d, prefix=P)
+    gb = make_grad(B, H, P + F * T, d, T * P + d)
+    masks = _masks(F, H, T + P)
+    print(f"[case] bwd mmdit d={d} T={T} P={P}", flush=True)
+    got = run_gpu_bwd_mmdit(qb, kb, vb, gb, masks, T, P, d ** -0.5)
+    ref = ommd.attention_backward_mmdit(qb, kb, vb, gb, masks, T, P, d ** -0.5)
+    for name, a, r in zip(("dq", "dk", "dv"), got, ref):
+        assert_grad(a, r, f"bwd-mmdit-d{d}-T{T}-P{P}-{name}")
+
+
+def test_bwd_mmdit_without_text_matches_plain_bitwise():
+    B, H, F, T, d = 1, 2, 5, 150, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=101)
+    gb = make_grad(B, H, F * T, d, 102)
+    mask = om.tile_mask(F, 1, "sym")
+    a = run_gpu_bwd_mmdit(qb, kb, vb, gb, mask, T, 0, d ** -0.5)
+    b = run_gpu_bwd(qb, kb, vb, gb, mask, T, d ** -0.5)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("k", [1, 12])
+def test_bwd_mmdit_cog_shape_sampled(k):
+    """CogVideoX-5B shape (226 text tokens, 13 x 1350 video tokens, 48 heads of 64),
+    sym masks: text and video query rows and key rows (text keys are kept by every
+    query) of two heads."""
+    w = workloads.WORKLOADS["cog"]
+    qb, kb, vb = workloads.make_workload_qkv(w)
+    gb = make_grad(w.B, w.H, w.S, w.d, 103)
+    mask = om.tile_mask(w.F, k, "sym")
+    print(f"[case] bwd cog k={k}", flush=True)
+    dq, dk, dv = run_gpu_bwd_mmdit(qb, kb, vb, gb, mask, w.T, w.prefix, w.scale())
+    rng = np.random.default_rng(k)
+    rows = []
+    for h in (0, w.H - 1):
+        for s in list(range(0, w.prefix, 37)) + [w.prefix - 1]:
+            rows.append((0, h, s))
+        for f in (0, 1, w.F - 1):
+            for r in {0, w.T - 1, int(rng.integers(0, w.T))}:
+                rows.append((0, h, w.prefix + f * w.T + r))
+    b, h, s = (np.array(x) for x in zip(*rows))
+    rq, rk, rv = ommd.attention_backward_mmdit_rows(qb, kb, vb, gb, mask, w.T, w.prefix, w.scale(),
+                                                    b, h, s, b, h, s)
+    assert_grad(dq[b, h, s], rq, f"cog-k{k}-dq")
+    assert_grad(dk[b, h, s], rk, f"cog-k{k}-dk")
+    assert_grad(dv[b, h, s], rv, f"cog-k{k}-dv")
