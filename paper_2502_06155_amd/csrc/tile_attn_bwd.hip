@@ -60,8 +60,15 @@ constexpr int kBwdThreads = 64 * kBwdWaves;
 // serialises the vector work) by 17% (dq) and 12% (dk/dv). At d = 128 the dk/dv
 // pass needs more than 256 registers and runs one workgroup per CU.
 constexpr int kRowsPerWg = kBwdWaves * 32;
+
+// What one launch of the key-side kernel produces. At d = 128 dK and dV together
+// (their accumulators, K and V operands alone take 192 registers) need one workgroup
+// per CU with the scores copied out of AGPRs; two passes that each fit 256 VGPRs
+// (dV: S and P only; dK: S, dP and dS) run at two workgroups per CU and, although
+// they form S twice (40 products instead of 32), take less time.
+enum KeyPass { kDkDv = 0, kDvOnly = 1, kDkOnly = 2 };
 template <int D>
-constexpr int dkdv_occupancy() { return D == 128 ? 1 : 2; }
+constexpr bool split_key_pass() { return D == 128; }
 
 template <int D>
 struct BShape {
@@ -392,9 +399,9 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
 
 // ---------------------------------------------------------------------------
 // dk/dv pass.
-template <int D, bool PREFIX>
-__global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_kernel(const BwdArgs a,
-                                                                                     int nkb) {
+template <int D, bool PREFIX, int MODE>
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs a, int nkb) {
+  constexpr bool kWantDv = MODE != kDkOnly, kWantDk = MODE != kDvOnly;
   using Sh = BShape<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t sQ[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sG[2][Sh::kTileElems];
@@ -427,17 +434,17 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   const bool wave_active = kblk * kRowsPerWg + wave * 32 < seg_len;
 
   // This lane's key as B operand of S = Q K^T and dP = dO V^T.
-  bf16x8 kf[Sh::kChunks], vf[Sh::kChunks];
+  bf16x8 kf[Sh::kChunks], vf[kWantDk ? Sh::kChunks : 1];
   const bool valid = krow < seg_len;
   const size_t kr = (size_t)bh * head_rows + seg0 + krow;
   load_row_operand<D>(a.k + kr * D, valid, a.keep, a.flip, hf, kf);
-  load_row_operand<D>(a.v + kr * D, valid, ~0u, 0u, hf, vf);
+  if constexpr (kWantDk) load_row_operand<D>(a.v + kr * D, valid, ~0u, 0u, hf, vf);
 
-  f32x16 dk[Sh::kDBlocks], dv[Sh::kDBlocks];
+  f32x16 dk[kWantDk ? Sh::kDBlocks : 1], dv[kWantDv ? Sh::kDBlocks : 1];
 #pragma unroll
   for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
-    dk[mb] = f32x16{};
-    dv[mb] = f32x16{};
+    if constexpr (kWantDk) dk[mb] = f32x16{};
+    if constexpr (kWantDv) dv[mb] = f32x16{};
   }
 
   const int tpf = (T + kBlockK - 1) / kBlockK;
@@ -462,8 +469,9 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
       if (wave == 0) {
         load_dword_to_lds(buffer_words(Lh + row0, (uint32_t)(nv * 4)), lds_addr((const uint16_t*)sL[bi]),
                           4 * lane);
-        load_dword_to_lds(buffer_words(Dh + row0, (uint32_t)(nv * 4)), lds_addr((const uint16_t*)sD[bi]),
-                          4 * lane);
+        if constexpr (kWantDk)
+          load_dword_to_lds(buffer_words(Dh + row0, (uint32_t)(nv * 4)), lds_addr((const uint16_t*)sD[bi]),
+                            4 * lane);
       }
     };
     SegmentCursor<PREFIX> cur, nxt;
@@ -481,7 +489,7 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
 #pragma unroll
       for (int cc = 0; cc < Sh::kChunks; ++cc) {
         sc = mfma32(row_frag<D>(sQ[buf], ra, qc, cc), kf[cc], sc);
-        dp = mfma32(row_frag<D>(sG[buf], ra, qc, cc), vf[cc], dp);
+        if constexpr (kWantDk) dp = mfma32(row_frag<D>(sG[buf], ra, qc, cc), vf[cc], dp);
       }
     };
     // P and dS of half qc as B operands (entry 8 c2 + 4u + j holds query row
@@ -494,7 +502,9 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sL[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
+          f32x4 d4 = {0.f, 0.f, 0.f, 0.f};
+          if constexpr (kWantDk)
+            d4 = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int e = 8 * c2 + 4 * u + j;
@@ -503,8 +513,8 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
             d8[4 * u + j] = p * (dp[e] - d4[j]);
           }
         }
-        pb[c2] = __builtin_convertvector(p8, bf16x8);
-        db[c2] = __builtin_convertvector(d8, bf16x8);
+        if constexpr (kWantDv) pb[c2] = __builtin_convertvector(p8, bf16x8);
+        if constexpr (kWantDk) db[c2] = __builtin_convertvector(d8, bf16x8);
       }
     };
     // dV^T += dO^T P and dK^T += Q^T dS over half qc.
@@ -513,8 +523,8 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
       for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
         for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
-          dv[mb] = mfma32(tr_frag<D>(sG[buf], ta, mb, 2 * qc + c2), pb[c2], dv[mb]);
-          dk[mb] = mfma32(tr_frag<D>(sQ[buf], ta, mb, 2 * qc + c2), db[c2], dk[mb]);
+          if constexpr (kWantDv) dv[mb] = mfma32(tr_frag<D>(sG[buf], ta, mb, 2 * qc + c2), pb[c2], dv[mb]);
+          if constexpr (kWantDk) dk[mb] = mfma32(tr_frag<D>(sQ[buf], ta, mb, 2 * qc + c2), db[c2], dk[mb]);
         }
     };
 
@@ -544,13 +554,13 @@ __global__ __launch_bounds__(kBwdThreads, dkdv_occupancy<D>()) void bwd_dkdv_ker
   // dK uses the unflipped q of the LDS tiles, so scale (with its sign) applies.
   if (krow < seg_len) {
     if (slot < 0) {
-      store_row_bf16<D>(a.dk + kr * D, dk, a.scale, hf);
-      store_row_bf16<D>(a.dv + kr * D, dv, 1.f, hf);
+      if constexpr (kWantDk) store_row_bf16<D>(a.dk + kr * D, dk, a.scale, hf);
+      if constexpr (kWantDv) store_row_bf16<D>(a.dv + kr * D, dv, 1.f, hf);
     } else {
       const int slot_rows = PREFIX ? max(T, a.P) : T;
       const size_t prow = ((size_t)slot * a.B + b) * slot_rows + krow;
-      store_row_f32<D>(a.ws_dk + prow * D, dk, a.scale, hf);
-      store_row_f32<D>(a.ws_dv + prow * D, dv, 1.f, hf);
+      if constexpr (kWantDk) store_row_f32<D>(a.ws_dk + prow * D, dk, a.scale, hf);
+      if constexpr (kWantDv) store_row_f32<D>(a.ws_dv + prow * D, dv, 1.f, hf);
     }
   }
 }
@@ -609,13 +619,27 @@ hipError_t dq_d(const BwdArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+template <int D, bool PREFIX, int MODE>
+void dkdv_launch(const BwdArgs& a, int nkb, hipStream_t stream) {
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, PREFIX, MODE>), dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream,
+                     a, nkb);
+}
+
+template <int D, bool PREFIX>
+void dkdv_passes(const BwdArgs& a, int nkb, hipStream_t stream) {
+  if constexpr (split_key_pass<D>()) {
+    dkdv_launch<D, PREFIX, kDvOnly>(a, nkb, stream);
+    dkdv_launch<D, PREFIX, kDkOnly>(a, nkb, stream);
+  } else {
+    dkdv_launch<D, PREFIX, kDkDv>(a, nkb, stream);
+  }
+}
+
 template <int D>
 hipError_t dkdv_d(const BwdArgs& a, hipStream_t stream) {
   const int nkb = (std::max(a.T, a.P) + kRowsPerWg - 1) / kRowsPerWg;
-  if (a.P > 0)
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, true>), dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream, a, nkb);
-  else
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, false>), dim3(a.n_wg_k), dim3(kBwdThreads), 0, stream, a, nkb);
+  if (a.P > 0) dkdv_passes<D, true>(a, nkb, stream);
+  else dkdv_passes<D, false>(a, nkb, stream);
   return hipGetLastError();
 }
 
