@@ -13,7 +13,8 @@
 //
 // Passes (all on the caller's stream)
 //   prep  lse in base 2 and delta per query row.
-//   dq    one workgroup per 128 query rows of a query frame, over the kept key
+//   dq    one workgroup per 128 query rows of a query frame (or of the text with a
+//         prefix, see Layout), over the kept key
 //         tiles (the forward's work list): S^T = K Q^T, dP^T = V dO^T,
 //         dQ^T += K^T dS^T. Each lane owns one query of its wave's 32-query
 //         column block, so lse and delta are per-lane constants.
@@ -27,7 +28,7 @@
 // through L2 at this shape, more than recomputing S and dP costs on the matrix cores.
 //
 // Both gradient kernels keep one operand of every product in registers (the
-// wave's 32 queries or 32 keys) and stream the other through LDS (see q_blocks
+// wave's 32 queries or 32 keys) and stream the other through LDS (see kRowsPerWg
 // below for why not 64 as in the forward kernel).
 //
 // LDS layout: every staged tile is read both row-wise (16 bytes per lane, 16

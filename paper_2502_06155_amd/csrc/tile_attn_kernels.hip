@@ -7,8 +7,10 @@
 //
 // Work decomposition
 //   One workgroup = 4 waves = 256 query rows of one (batch, head, query frame);
-//   each wave owns 64 rows as two 32-query column blocks. Query blocks are frame
-//   aligned, so every row of a workgroup shares one kept list. Workgroup ids are
+//   each wave owns 64 rows as two 32-query column blocks (128 rows and one block
+//   at d = 128, see fwd_q_blocks). Query blocks are frame aligned, so every row of
+//   a workgroup shares one kept list. With a text prefix (the MM-DiT form) the text
+//   is one more segment, see Layout. Workgroup ids are
 //   remapped so that each XCD (8 per MI355X, each with its own L2) receives a
 //   contiguous run of (batch, head) problems, which keeps the K/V of the shared
 //   global frames resident in that XCD's L2. Two workgroups share a CU, so each
