@@ -31,10 +31,13 @@
  *   - Thread-safe. The first call for a given mask (per device) uploads its
  *     work plan (tile_attn_plan) with a blocking allocation and copy. A mask
  *     whose plan splits heavy query frames also needs a workspace for the
- *     partial results, n_slots * B * H * T * (d + 1) * 4 bytes, held per
- *     (device, stream) and grown (with a wait on that stream) when a call needs
- *     more. Later calls that fit allocate nothing and do not synchronise, so a
- *     warmed-up call can be captured in a HIP graph.
+ *     partial results, n_slots * B * max(T, P) * (d + 1) * 4 bytes (n_slots
+ *     counts the pieces of all heads), held per (device, stream). A call that
+ *     needs more allocates a larger one (at least 1.5 times the size) and keeps
+ *     the old one allocated until process exit, so no enqueued work ever sees
+ *     its workspace freed and growing never waits for the stream. Later calls
+ *     that fit allocate nothing and do not synchronise, so a warmed-up call can
+ *     be captured in a HIP graph.
  */
 #ifndef TILE_ATTN_H
 #define TILE_ATTN_H

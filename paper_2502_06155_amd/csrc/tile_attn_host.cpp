@@ -114,10 +114,12 @@ std::mutex g_cache_mutex;
 std::map<std::pair<int, std::string>, DeviceWorkList> g_cache;
 
 // Partial-result workspace of split frames, one per (device, stream) so that calls
-// on different streams never share it; grown on demand, kept until process exit.
+// on different streams never share it; replaced by a larger one on demand, every
+// buffer kept until process exit.
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
+  std::vector<void*> retired;
 };
 std::map<std::pair<int, void*>, Workspace> g_workspaces;
 
@@ -217,20 +219,27 @@ int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_sp
   return TA_OK;
 }
 
-// Workspace of at least `bytes` for (dev, stream). Growing it waits for the
-// stream, whose earlier calls may still be using the old one.
+// Workspace of at least `bytes` for (dev, stream). One that is too small is replaced
+// by a larger one (at least 1.5 times the old size, so replacements stay few) and
+// kept allocated until process exit: work already enqueued with it, or being
+// enqueued by another thread that was handed it, never sees it freed, and nothing
+// has to wait for the stream.
 int workspace_for(int dev, void* stream, size_t bytes, void** out) {
   std::lock_guard<std::mutex> lock(g_cache_mutex);
   Workspace& ws = g_workspaces[{dev, stream}];
   if (ws.bytes < bytes) {
-    hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipStreamSynchronize: ") + hipGetErrorString(e));
-    if (ws.ptr) (void)hipFree(ws.ptr);
-    ws.ptr = nullptr;
-    ws.bytes = 0;
-    e = hipMalloc(&ws.ptr, bytes);
+    size_t size = std::max(bytes, ws.bytes + ws.bytes / 2);
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, size);
+    if (e != hipSuccess && size > bytes) {
+      (void)hipGetLastError();
+      size = bytes;  // the geometric size may not fit where the exact one does
+      e = hipMalloc(&p, size);
+    }
     if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
-    ws.bytes = bytes;
+    if (ws.ptr) ws.retired.push_back(ws.ptr);
+    ws.ptr = p;
+    ws.bytes = size;
   }
   *out = ws.ptr;
   return TA_OK;
