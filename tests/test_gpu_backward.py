@@ -316,3 +316,54 @@ def test_bwd_mmdit_cog_shape_sampled(k):
     assert_grad(dq[b, h, s], rq, f"cog-k{k}-dq")
     assert_grad(dk[b, h, s], rk, f"cog-k{k}-dk")
     assert_grad(dv[b, h, s], rv, f"cog-k{k}-dv")
+
+
+def test_all_zero_mask_forward_and_gradients():
+    """A mask that keeps nothing: zero output, -inf log-sum-exp, zero gradients (every
+    output written over a NaN fill)."""
+    B, H, F, T, d = 1, 2, 3, 100, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=110)
+    gb = make_grad(B, H, F * T, d, 111)
+    mask = np.zeros((F, F), np.uint8)
+    q, k, v, g = (to_dev(x) for x in (qb, kb, vb, gb))
+    out = torch.full_like(q, float("nan"))
+    lse = torch.zeros((B, H, F * T), dtype=torch.float32, device="cuda")
+    ta.tile_attn_fwd_heads(q, k, v, out, B, H, F, T, d, mask, 0.125, lse, None)
+    grads = [torch.full_like(q, float("nan")) for _ in range(3)]
+    ta.tile_attn_bwd(q, k, v, out, g, lse, *grads, B, H, F, T, d, mask, 0.125, None)
+    torch.cuda.synchronize()
+    assert not np.any(widen(from_dev(out)))
+    assert np.all(np.isneginf(lse.cpu().numpy()))
+    for x in grads:
+        assert not np.any(widen(from_dev(x)))
+
+
+def test_calls_of_growing_size_share_one_stream_without_waits():
+    """Forward and gradient calls of increasing workspace needs queued back to back on
+    one stream (each grows the workspace; the old ones stay alive): every result
+    matches the oracle."""
+    d, scale = 64, 0.125
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    cases = [(1, 2, 6, 90, "sym"), (2, 2, 8, 150, "col"), (1, 3, 10, 200, "sym")]
+    results = []
+    with torch.cuda.stream(s):
+        for (B, H, F, T, form) in cases:
+            qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=F * T)
+            gb = make_grad(B, H, F * T, d, F + T)
+            mask = om.tile_mask(F, 1, form)
+            q, k, v, g = (to_dev(x) for x in (qb, kb, vb, gb))
+            out = torch.empty_like(q)
+            lse = torch.empty((B, H, F * T), dtype=torch.float32, device="cuda")
+            grads = [torch.empty_like(q) for _ in range(3)]
+            ta.tile_attn_fwd_heads(q, k, v, out, B, H, F, T, d, mask, scale, lse, s)
+            ta.tile_attn_bwd(q, k, v, out, g, lse, *grads, B, H, F, T, d, mask, scale, s)
+            results.append((qb, kb, vb, gb, mask, T, out, grads))
+    torch.cuda.synchronize()
+    for qb, kb, vb, gb, mask, T, out, grads in results:
+        from oracle import attention as oa
+        from tests.gpu_helpers import assert_parity
+        assert_parity(from_dev(out), oa.attention(qb, kb, vb, mask, T, scale), "stream-fwd")
+        ref = ob.attention_backward(qb, kb, vb, gb, mask, T, scale)
+        for name, a, r in zip(("dq", "dk", "dv"), grads, ref):
+            assert_grad(from_dev(a), r, f"stream-{name}")
