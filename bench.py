@@ -102,6 +102,18 @@ def traffic_from_profile(which: str = "fwd"):
     return float(rec["hbm_bytes_per_launch"])
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), for the baseline's record."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
 def cpu_baseline(w, qb, kb, vb, mask, budget_s: float):
     """Time the float64 oracle on whole heads of the same problem until the budget
     is spent; report kept TFLOP/s of that sample."""
@@ -132,7 +144,7 @@ def cpu_baseline(w, qb, kb, vb, mask, budget_s: float):
         "cores": int(threads),
         "kind": "oracle",
         "sample": f"float64 oracle on heads 0..{done - 1} of {w.H} (all {w.F} query frames, "
-                  f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles",
+                  f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles; {cpu_model()}",
     }
 
 
@@ -167,7 +179,7 @@ def cpu_baseline_bwd(w, qb, kb, vb, gb, mask, budget_s: float):
         "cores": int(threads),
         "kind": "oracle",
         "sample": f"float64 gradient oracle on heads 0..{done - 1} of {w.H} (all {w.F} frames, "
-                  f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles",
+                  f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles; {cpu_model()}",
     }
 
 
@@ -294,8 +306,9 @@ def run_all(args, torch, ta):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    # the paper's protocol (Sec. 4.2.1): 25 warm-up calls, then 100 timed ones
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--workload", default="93f", choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--form", default="col", choices=["col", "sym", "dense"])
     ap.add_argument("--g", type=int, default=None)
