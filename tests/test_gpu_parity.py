@@ -377,3 +377,58 @@ def test_per_head_masks_full_size_sampled():
     for hh in (0, 5):
         ref_lse = oa.attention_lse(qb[:, hh:hh + 1], kb[:, hh:hh + 1], masks[hh], w.T, w.scale())
         assert_lse(lse[:, hh:hh + 1], ref_lse, f"heads-93f-lse-h{hh}")
+
+
+def test_hip_graph_capture_and_replay():
+    """A warmed-up call (its work list uploaded and its workspace sized on the capture
+    stream) records into a HIP graph: forward with split rows (attention kernel and
+    merge) and the gradients. Several replays, with eager work and synchronisation
+    between them, each equal the eager result bit for bit."""
+    B, H, F, T, d = 1, 2, 10, 100, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=120)
+    rng = np.random.default_rng(121)
+    gb = workloads.f32_to_bf16_bits(rng.standard_normal(qb.shape).astype(np.float32))
+    mask = om.tile_mask(F, 1, "sym")
+    assert ta.tile_attn_plan(mask)[1] > 0 and ta.tile_attn_plan(mask.T.copy())[1] > 0  # splits on both sides
+    scale = d ** -0.5
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        q, k, v, g = (to_dev(x) for x in (qb, kb, vb, gb))
+        out = torch.empty_like(q)
+        lse = torch.empty((B, H, F * T), dtype=torch.float32, device="cuda")
+        grads = [torch.empty_like(q) for _ in range(3)]
+
+    def step():
+        ta.tile_attn_fwd_heads(q, k, v, out, B, H, F, T, d, mask, scale, lse, s)
+        ta.tile_attn_bwd(q, k, v, out, g, lse, *grads, B, H, F, T, d, mask, scale, s)
+
+    with torch.cuda.stream(s):
+        for _ in range(2):
+            step()
+    s.synchronize()
+    eager = [from_dev(x) for x in [out] + grads]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        step()
+    for rep in range(3):
+        for x in [out] + grads:
+            x.fill_(float("nan"))  # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, e in zip([from_dev(x) for x in [out] + grads], eager):
+            assert np.array_equal(a, e), rep
+    assert_parity(eager[0], oa.attention(qb, kb, vb, mask, T, scale), "graph-fwd")
+
+
+def test_max_frames():
+    """F = TA_MAX_FRAMES (1024) with tiny frames: a random sparse mask with some full
+    rows (split) and empty rows, through the forward."""
+    B, H, F, T, d = 1, 2, 1024, 3, 64
+    rng = np.random.default_rng(130)
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=130)
+    mask = (rng.random((F, F)) < 0.01).astype(np.uint8)
+    mask[::97, :] = 1
+    mask[5::211, :] = 0
+    full_check(qb, kb, vb, mask, T, d ** -0.5, "max-frames")
