@@ -396,20 +396,33 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
 #pragma unroll
           for (int qs = 0; qs < QB; ++qs) mask_tail(s0[qs], 0, hf, nvalid);
         }
+        // Two regions: QK^T of block 1 with the weights of block 0, then PV of block 0
+        // with the weights of block 1. Each holds QB * D/16 MFMAs and about 48 QB
+        // vector instructions (per element: fma, exp, half a conversion, half a dot2).
+        // At d = 96 and 128 the regions are fenced and the vector work is spread
+        // evenly between the MFMAs (3% faster than the scheduler's own order); at
+        // d = 64 the unfenced interleave with LDS reads measured 1-2% better.
+        constexpr bool kFence = D != 64;
+        constexpr int kMfma = QB * (D / 16), kValuPerMfma = 768 / D;
+        if constexpr (kFence) __builtin_amdgcn_sched_barrier(0);
         qk_block<D, QB>(sK[buf], qf, ka, 1, s1);
 #pragma unroll
         for (int qs = 0; qs < QB; ++qs) l0[qs] = block_weights(s0[qs], c, m_ref[qs] * c, p0[qs]);
-        interleave_mfma_valu<QB * (D / 16), 24 * QB>();
+        if constexpr (kFence) spread_valu_over_mfma<kMfma, kValuPerMfma>();
+        else interleave_mfma_valu<kMfma, 24 * QB>();
         check_block(s0, p0, l0);
         if (nvalid < kBlockK) {
 #pragma unroll
           for (int qs = 0; qs < QB; ++qs) mask_tail(s1[qs], 1, hf, nvalid);
         }
+        if constexpr (kFence) __builtin_amdgcn_sched_barrier(0);
         pv_block<D, QB>(sV[buf], p0, va, 0, o);
 #pragma unroll
         for (int qs = 0; qs < QB; ++qs) l1[qs] = block_weights(s1[qs], c, m_ref[qs] * c, p1[qs]);
-        interleave_mfma_valu<QB * (D / 16), 24 * QB>();
+        if constexpr (kFence) spread_valu_over_mfma<kMfma, kValuPerMfma>();
+        else interleave_mfma_valu<kMfma, 24 * QB>();
         check_block(s1, p1, l1);
+        if constexpr (kFence) __builtin_amdgcn_sched_barrier(0);
         pv_block<D, QB>(sV[buf], p1, va, 1, o);
       }
       cur = nxt;

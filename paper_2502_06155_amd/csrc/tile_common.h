@@ -149,8 +149,7 @@ __device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
 
 // Scheduling hint for a region holding N_MFMA matrix instructions (with their LDS
 // fragment reads) and about N_VALU vector instructions that do not depend on
-// them: each MFMA is followed by a share of the VALU work, so the vector ALUs
-// issue while the matrix core runs.
+// them: each MFMA is followed by a share of the VALU work and one LDS read.
 template <int N_MFMA, int N_VALU>
 __device__ __forceinline__ void interleave_mfma_valu() {
   __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
@@ -159,6 +158,20 @@ __device__ __forceinline__ void interleave_mfma_valu() {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
     __builtin_amdgcn_sched_group_barrier(0x002, (N_VALU + N_MFMA - 1) / N_MFMA, 0);  // VALU
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                        // DS read
+  }
+}
+
+// Scheduling hint for a region holding N_MFMA matrix instructions and about
+// N_MFMA * VALU_PER vector instructions that do not depend on them: each MFMA is
+// followed by VALU_PER vector instructions, so the vector ALUs issue while the
+// matrix core runs (LDS reads are left to the scheduler). Used between scheduling
+// fences that keep the region to those instructions.
+template <int N_MFMA, int VALU_PER>
+__device__ __forceinline__ void spread_valu_over_mfma() {
+#pragma unroll
+  for (int i = 0; i < N_MFMA; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);         // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, VALU_PER, 0);  // VALU
   }
 }
 
