@@ -54,13 +54,14 @@ hipError_t launch_tile_attn_fwd(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_merge_partials(const MergeArgs& a, hipStream_t stream);
 
 // Gradients. The prep pass turns the forward's natural-log log-sum-exp into base 2
-// and forms delta = <dO, out> per query row.
+// and forms ndelta = -<dO, out> per query row (negated: the dq pass starts its dP^T
+// accumulations at it, so dP - delta comes out of the matrix cores).
 struct PrepArgs {
   const uint16_t* out;
   const uint16_t* dout;
   const float* lse;  // natural log, [rows]
   float* lse2;       // base 2, [rows]
-  float* delta;      // [rows]
+  float* ndelta;     // [rows]
   int64_t rows;      // B * H * F * T
   int d;
 };
@@ -81,7 +82,7 @@ struct BwdArgs {
   int B, H, F, T, d;
   int P;  // text tokens before the video (0: none); segments as in FwdArgs
   const float* lse2;
-  const float* delta;
+  const float* ndelta;
   const int32_t* items_q;
   const int32_t* cols_q;
   int n_items_q;

@@ -12,12 +12,13 @@
 // tiles are never read here either.
 //
 // Passes (all on the caller's stream)
-//   prep  lse in base 2 and delta per query row.
+//   prep  lse in base 2 and -delta per query row (the dq pass starts its dP^T
+//         accumulations at -delta, so dP - delta takes no vector op there).
 //   dq    one workgroup per 128 query rows of a query frame (or of the text with a
 //         prefix, see Layout), over the kept key
 //         tiles (the forward's work list): S^T = K Q^T, dP^T = V dO^T,
 //         dQ^T += K^T dS^T. Each lane owns one query of its wave's 32-query
-//         column block, so lse and delta are per-lane constants.
+//         column block, so lse and -delta are per-lane constants.
 //   dkdv  one workgroup per 128 key rows of a key frame, over the query tiles of
 //         the frames that keep it (the work list of the transposed mask):
 //         S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dS. Each lane owns
@@ -201,7 +202,7 @@ __device__ __forceinline__ void store_row_f32(float* row, const f32x16 (&acc)[D 
 }
 
 // ---------------------------------------------------------------------------
-// prep: lse2 = lse * log2(e), delta = <dO, out> (fp32 sum of bf16 products).
+// prep: lse2 = lse * log2(e), ndelta = -<dO, out> (fp32 sum of bf16 products).
 // One workgroup per 64 rows: the 256 threads read the rows' 16-byte pieces
 // contiguously (coalesced), leave per-piece partial dots in LDS, and 64 threads
 // add up one row each.
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restric
                                                        const uint16_t* __restrict__ dout,
                                                        const float* __restrict__ lse,
                                                        float* __restrict__ lse2,
-                                                       float* __restrict__ delta, int64_t rows) {
+                                                       float* __restrict__ ndelta, int64_t rows) {
   constexpr int kPieces = D / 8;
   constexpr int kPerThread = kPrepRows * kPieces / 256;
   static_assert(kPrepRows * kPieces == 256 * kPerThread, "whole pieces per thread");
@@ -238,7 +239,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t* __restric
 #pragma unroll
     for (int c = 0; c < kPieces; ++c) acc += part[threadIdx.x * kPieces + c];
     const int64_t r = row0 + threadIdx.x;
-    delta[r] = acc;
+    ndelta[r] = -acc;
     lse2[r] = lse[r] * 1.4426950408889634f;
   }
 }
@@ -257,16 +258,17 @@ __device__ __forceinline__ float prob(float s, float c, float lse2) {
 // dq pass.
 //
 // dS^T of one 32-key block for one column block, as the B operand of
-// dQ^T += K^T dS^T: entries 8c2 .. 8c2+7 of the C fragment.
+// dQ^T += K^T dS^T: entries 8c2 .. 8c2+7 of the C fragment. dp already holds
+// dP - delta (its accumulation started at -delta).
 __device__ __forceinline__ void dq_scores(const f32x16& s, const f32x16& dp, float c, float lse2,
-                                          float dlt, bf16x8 (&ds)[2]) {
+                                          bf16x8 (&ds)[2]) {
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2) {
     f32x8 x;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float p = prob(s[8 * c2 + e], c, lse2);
-      x[e] = p * (dp[8 * c2 + e] - dlt);
+      x[e] = p * dp[8 * c2 + e];
     }
     ds[c2] = __builtin_convertvector(x, bf16x8);
   }
@@ -302,14 +304,18 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
   const int qrow = qb * kRowsPerWg + wave * 32 + n;
   const bool wave_active = qb * kRowsPerWg + wave * 32 < seg_len;
 
-  // This lane's query: Q^T and dO^T B-operand slices, its lse (base 2) and delta.
+  // This lane's query: Q^T and dO^T B-operand slices, its lse (base 2) and -delta,
+  // the start of every dP^T accumulation.
   bf16x8 qf[Sh::kChunks], gf[Sh::kChunks];
   const bool valid = qrow < seg_len;
   const size_t qr = (size_t)bh * head_rows + seg0 + qrow;
   load_row_operand<D>(a.q + qr * D, valid, a.keep, a.flip, hf, qf);
   load_row_operand<D>(a.dout + qr * D, valid, ~0u, 0u, hf, gf);
   const float lse2 = valid ? a.lse2[qr] : 0.f;
-  const float dlt = valid ? a.delta[qr] : 0.f;
+  const float ndlt = valid ? a.ndelta[qr] : 0.f;
+  f32x16 dp_start;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) dp_start[e] = ndlt;
 
   f32x16 acc[Sh::kDBlocks];
 #pragma unroll
@@ -337,11 +343,11 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
     wait_tile_loads();
     __syncthreads();
 
-    // S^T and dP^T of 32-key block kb (raw logits; keys past the tile's valid rows
-    // read zero rows).
+    // S^T and dP^T - delta of 32-key block kb (raw logits; keys past the tile's valid
+    // rows read zero rows).
     auto scores = [&](const uint16_t* tk, const uint16_t* tv, int kb, f32x16& sc, f32x16& dp) {
       sc = f32x16{};
-      dp = f32x16{};
+      dp = dp_start;
 #pragma unroll
       for (int cc = 0; cc < Sh::kChunks; ++cc) {
         sc = mfma32(row_frag<D>(tk, ra, kb, cc), qf[cc], sc);
@@ -373,10 +379,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
         scores(sK[buf], sV[buf], 0, s0, dp0);
         __builtin_amdgcn_sched_barrier(0);
         scores(sK[buf], sV[buf], 1, s1, dp1);
-        dq_scores(s0, dp0, a.c, lse2, dlt, ds0);
+        dq_scores(s0, dp0, a.c, lse2, ds0);
         __builtin_amdgcn_sched_barrier(0);
         accumulate(sK[buf], 0, ds0);
-        dq_scores(s1, dp1, a.c, lse2, dlt, ds1);
+        dq_scores(s1, dp1, a.c, lse2, ds1);
         __builtin_amdgcn_sched_barrier(0);
         accumulate(sK[buf], 1, ds1);
       }
@@ -426,7 +432,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
   const uint16_t* Qh = a.q + bh * head_rows * D;
   const uint16_t* Gh = a.dout + bh * head_rows * D;
   const float* Lh = a.lse2 + bh * head_rows;
-  const float* Dh = a.delta + bh * head_rows;
+  const float* Dh = a.ndelta + bh * head_rows;
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
@@ -460,7 +466,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
     ra.init(n, hf);
     TrAddr<D> ta;
     ta.init(lane);
-    // Q, dO, lse2 and delta of one 64-query tile; rows past the valid range read
+    // Q, dO, lse2 and -delta of one 64-query tile; rows past the valid range read
     // as zeros, so they add exactly nothing below (zero Q and dO rows, P <= 1).
     auto load_tile = [&](const SegmentCursor<PREFIX>& tc, int bi) {
       const size_t row0 = tc.key0();
@@ -503,15 +509,15 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sL[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
-          f32x4 d4 = {0.f, 0.f, 0.f, 0.f};
+          f32x4 nd4 = {0.f, 0.f, 0.f, 0.f};
           if constexpr (kWantDk)
-            d4 = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
+            nd4 = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int e = 8 * c2 + 4 * u + j;
             const float p = prob(sc[e], a.c, l4[j]);
             p8[4 * u + j] = p;
-            d8[4 * u + j] = p * (dp[e] - d4[j]);
+            d8[4 * u + j] = p * (dp[e] + nd4[j]);
           }
         }
         if constexpr (kWantDv) pb[c2] = __builtin_convertvector(p8, bf16x8);
@@ -606,7 +612,7 @@ template <int D>
 hipError_t prep_d(const PrepArgs& a, hipStream_t stream) {
   const int64_t blocks = (a.rows + kPrepRows - 1) / kPrepRows;
   hipLaunchKernelGGL(bwd_prep_kernel<D>, dim3((uint32_t)blocks), dim3(256), 0, stream, a.out, a.dout,
-                     a.lse, a.lse2, a.delta, a.rows);
+                     a.lse, a.lse2, a.ndelta, a.rows);
   return hipGetLastError();
 }
 

@@ -391,8 +391,8 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
   st = workspace_for(dev, stream, bytes, &ws);
   if (st != TA_OK) return st;
   float* lse2 = static_cast<float*>(ws);
-  float* delta = lse2 + rows;
-  float* ws_dq = delta + rows;
+  float* ndelta = lse2 + rows;
+  float* ws_dq = ndelta + rows;
   float* ws_dk = ws_dq + (size_t)wq->n_slots * B * L * d;
   float* ws_dv = ws_dk + (size_t)wk->n_slots * B * L * d;
   const hipStream_t s = static_cast<hipStream_t>(stream);
@@ -402,7 +402,7 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
   pa.dout = static_cast<const uint16_t*>(dout);
   pa.lse = lse;
   pa.lse2 = lse2;
-  pa.delta = delta;
+  pa.ndelta = ndelta;
   pa.rows = (int64_t)rows;
   pa.d = d;
   e = ta::launch_bwd_prep(pa, s);
@@ -423,7 +423,7 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
   a.d = d;
   a.P = P;
   a.lse2 = lse2;
-  a.delta = delta;
+  a.ndelta = ndelta;
   a.items_q = wq->items;
   a.cols_q = wq->cols;
   a.n_items_q = wq->n_items;
