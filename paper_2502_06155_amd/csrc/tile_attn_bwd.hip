@@ -40,6 +40,8 @@
 // the rows' 64-byte quads in different bank groups.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include <float.h>
 #include <stdint.h>
 
@@ -363,8 +365,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
           acc[mb] = mfma32(tr_frag<D>(tk, ta, mb, 2 * kb + c2), ds[c2], acc[mb]);
     };
 
-    for (int t = 0; t < n_tiles; ++t) {
-      const int buf = t & 1;
+    // One tile; the buffer index is a compile-time constant (tiles run in pairs), so
+    // every LDS address is a per-lane base plus an immediate offset.
+    auto tile_step = [&](auto bufc, int t) {
+      constexpr int buf = decltype(bufc)::value;
       if (t + 1 < n_tiles) {
         ld.load(Kh, nxt.key0(), nxt.nvalid(), sK[buf ^ 1], wave);
         ld.load(Vh, nxt.key0(), nxt.nvalid(), sV[buf ^ 1], wave);
@@ -390,6 +394,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
       nxt.advance(n_kept);
       wait_tile_loads();
       __syncthreads();
+    };
+    for (int t = 0; t < n_tiles; t += 2) {
+      tile_step(std::integral_constant<int, 0>{}, t);
+      if (t + 1 < n_tiles) tile_step(std::integral_constant<int, 1>{}, t + 1);
     }
   }
 
@@ -535,8 +543,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
         }
     };
 
-    for (int t = 0; t < n_tiles; ++t) {
-      const int buf = t & 1;
+    // One tile; the buffer index is a compile-time constant (the loop below runs tiles
+    // in pairs), so every LDS address is a per-lane base plus an immediate offset.
+    auto tile_step = [&](auto bufc, int t) {
+      constexpr int buf = decltype(bufc)::value;
       if (t + 1 < n_tiles) load_tile(nxt, buf ^ 1);
       if (wave_active) {
         // Program order puts half 1's S/dP ahead of half 0's P and dS and half 0's
@@ -555,6 +565,10 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
       nxt.advance(n_keep);
       wait_tile_loads();
       __syncthreads();
+    };
+    for (int t = 0; t < n_tiles; t += 2) {
+      tile_step(std::integral_constant<int, 0>{}, t);
+      if (t + 1 < n_tiles) tile_step(std::integral_constant<int, 1>{}, t + 1);
     }
   }
 

@@ -49,12 +49,15 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 template <bool PREFIX>
 struct Layout {
   int F, T, P;
+  // Written as arithmetic on the fields' values: a conditional choice between two
+  // fields can become a load through a chosen address, which keeps the whole
+  // struct (and a cursor holding it) in scratch memory instead of registers.
   __device__ __forceinline__ int start(int j) const {
-    if constexpr (PREFIX) return j < F ? P + j * T : 0;
+    if constexpr (PREFIX) return (j < F) * (P + j * T);
     else return j * T;
   }
   __device__ __forceinline__ int len(int j) const {
-    if constexpr (PREFIX) return j < F ? T : P;
+    if constexpr (PREFIX) return P + (j < F) * (T - P);
     else return T;
   }
 };
