@@ -53,6 +53,7 @@
 #include <float.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <stdint.h>
 
 #include "launch.h"
@@ -375,8 +376,10 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
       for (int qs = 0; qs < QB; ++qs) l_run[qs] += ls[qs];
     };
 
-    for (int t = 0; t < n_tiles; ++t) {
-      const int buf = t & 1;
+    // One tile; the buffer index is a compile-time constant (the loop below runs tiles
+    // in pairs), so every LDS address is a per-lane base plus an immediate offset.
+    auto tile_step = [&](auto bufc, int t) {
+      constexpr int buf = decltype(bufc)::value;
       // Tile t+1 lands in the buffers tile t-1 freed (all waves passed the last
       // barrier) while tile t is consumed.
       if (t + 1 < n_tiles) {
@@ -429,6 +432,10 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
       nxt.advance(n_kept);
       wait_tile_loads();
       __syncthreads();
+    };
+    for (int t = 0; t < n_tiles; t += 2) {
+      tile_step(std::integral_constant<int, 0>{}, t);
+      if (t + 1 < n_tiles) tile_step(std::integral_constant<int, 1>{}, t + 1);
     }
   }
 
