@@ -216,7 +216,11 @@ def test_bwd_last_key_block_full_frames():
     full_check(qb, kb, vb, gb, om.tile_mask(F, 1, "col"), T, d ** -0.5, "bwd-3600")
 
 
-FULL_CASES = [("93f", "col", 1), ("93f", "sym", 1), ("29f", "col", 1)]
+# Every workload the benchmark times for the gradients: the 93-frame and 29-frame shapes,
+# the frame-correlated sweep data, one GPU's head share, the 48-frame long horizon (T =
+# 1200, two global frames) and 128-wide heads (split dV and dK key-side passes).
+FULL_CASES = [("93f", "col", 1), ("93f", "sym", 1), ("29f", "col", 1), ("sweep", "sym", 2),
+              ("sp_share", "sym", 1), ("long", "col", 2), ("93f_d128", "col", 1)]
 
 
 @pytest.mark.parametrize("name,form,g", FULL_CASES, ids=[f"{a}-{b}-g{c}" for a, b, c in FULL_CASES])
