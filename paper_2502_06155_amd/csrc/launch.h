@@ -54,8 +54,8 @@ hipError_t launch_tile_attn_fwd(const FwdArgs& a, hipStream_t stream);
 hipError_t launch_merge_partials(const MergeArgs& a, hipStream_t stream);
 
 // Gradients. The prep pass turns the forward's natural-log log-sum-exp into base 2
-// and forms ndelta = -<dO, out> per query row (negated: the dq pass starts its dP^T
-// accumulations at it, so dP - delta comes out of the matrix cores).
+// and forms ndelta = -<dO, out> per query row (negated: both gradient kernels start
+// their dP accumulations at it, so dP - delta comes out of the matrix cores).
 struct PrepArgs {
   const uint16_t* out;
   const uint16_t* dout;

@@ -12,8 +12,8 @@
 // tiles are never read here either.
 //
 // Passes (all on the caller's stream)
-//   prep  lse in base 2 and -delta per query row (the dq pass starts its dP^T
-//         accumulations at -delta, so dP - delta takes no vector op there).
+//   prep  lse in base 2 and -delta per query row (both gradient kernels start
+//         their dP accumulations at -delta, so dP - delta takes no vector op).
 //   dq    one workgroup per 128 query rows of a query frame (or of the text with a
 //         prefix, see Layout), over the kept key
 //         tiles (the forward's work list): S^T = K Q^T, dP^T = V dO^T,
@@ -497,15 +497,28 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
     wait_tile_loads();
     __syncthreads();
 
-    // S and dP of 32-query half qc of the tile.
-    auto scores = [&](int buf, int qc, f32x16& sc, f32x16& dp) {
-      sc = f32x16{};
-      dp = f32x16{};
+    // dP - delta of 32-query half qc of the tile: the accumulation starts at the rows' -delta
+    // (entry 8 c2 + 4u + j holds query row 32 qc + 16 c2 + 8u + 4h + j), read before
+    // both halves' S so that the reads land while S forms.
+    auto dp_start = [&](int buf, int qc, f32x16& dp) {
 #pragma unroll
-      for (int cc = 0; cc < Sh::kChunks; ++cc) {
-        sc = mfma32(row_frag<D>(sQ[buf], ra, qc, cc), kf[cc], sc);
-        if constexpr (kWantDk) dp = mfma32(row_frag<D>(sG[buf], ra, qc, cc), vf[cc], dp);
-      }
+      for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dp[8 * c2 + 4 * u + j] = d4[j];
+        }
+    };
+    // S of half qc.
+    auto s_chain = [&](int buf, int qc, f32x16& sc) {
+      sc = f32x16{};
+#pragma unroll
+      for (int cc = 0; cc < Sh::kChunks; ++cc) sc = mfma32(row_frag<D>(sQ[buf], ra, qc, cc), kf[cc], sc);
+    };
+    auto dp_chain = [&](int buf, int qc, f32x16& dp) {
+#pragma unroll
+      for (int cc = 0; cc < Sh::kChunks; ++cc) dp = mfma32(row_frag<D>(sG[buf], ra, qc, cc), vf[cc], dp);
     };
     // P and dS of half qc as B operands (entry 8 c2 + 4u + j holds query row
     // 32 qc + 16 c2 + 8u + 4h + j).
@@ -517,15 +530,12 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sL[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
-          f32x4 nd4 = {0.f, 0.f, 0.f, 0.f};
-          if constexpr (kWantDk)
-            nd4 = *reinterpret_cast<const f32x4*>(&sD[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int e = 8 * c2 + 4 * u + j;
             const float p = prob(sc[e], a.c, l4[j]);
             p8[4 * u + j] = p;
-            d8[4 * u + j] = p * (dp[e] + nd4[j]);
+            d8[4 * u + j] = p * dp[e];  // dp holds dP - delta
           }
         }
         if constexpr (kWantDv) pb[c2] = __builtin_convertvector(p8, bf16x8);
@@ -549,13 +559,22 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
       constexpr int buf = decltype(bufc)::value;
       if (t + 1 < n_tiles) load_tile(nxt, buf ^ 1);
       if (wave_active) {
-        // Program order puts half 1's S/dP ahead of half 0's P and dS and half 0's
-        // dV/dK update ahead of half 1's P and dS; the compiler interleaves them
-        // (fencing the phases, as in the dq pass, measured 4% slower here).
+        // Program order: both halves' -delta reads, S, then dP (so the reads land
+        // while S forms), then half 0's P and dS and dV/dK update ahead of half 1's
+        // P and dS; the compiler interleaves them (fencing the phases, as in the dq
+        // pass, measured 4% slower here).
         f32x16 s0, dp0, s1, dp1;
         bf16x8 pb0[2], db0[2], pb1[2], db1[2];
-        scores(buf, 0, s0, dp0);
-        scores(buf, 1, s1, dp1);
+        if constexpr (kWantDk) {
+          dp_start(buf, 0, dp0);
+          dp_start(buf, 1, dp1);
+        }
+        s_chain(buf, 0, s0);
+        s_chain(buf, 1, s1);
+        if constexpr (kWantDk) {
+          dp_chain(buf, 0, dp0);
+          dp_chain(buf, 1, dp1);
+        }
         grads(buf, 0, s0, dp0, pb0, db0);
         accumulate(buf, 0, pb0, db0);
         grads(buf, 1, s1, dp1, pb1, db1);
