@@ -252,6 +252,28 @@ __device__ __forceinline__ float block_weights(const f32x16& s, float c, float m
   return ls;
 }
 
+// The weights of keys 2e and 2e+1 of chunk c2 of a 32-key block for one column
+// block, exactly as block_weights forms them: one packed dword of the B operand,
+// and their bf16 values added to this lane's sum.
+__device__ __forceinline__ void pair_weights(const f32x16& s, int c2, int e, float c, float mc,
+                                             u32x4& pw, float& ls) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  const f32x2 x = {fast_exp2(__builtin_fmaf(s[8 * c2 + 2 * e], c, -mc)),
+                   fast_exp2(__builtin_fmaf(s[8 * c2 + 2 * e + 1], c, -mc))};
+  const bf16x2 y = __builtin_convertvector(x, bf16x2);
+  pw[e] = __builtin_bit_cast(uint32_t, y);
+  ls = __builtin_amdgcn_fdot2_f32_bf16(y, ones, ls, false);
+}
+
+// fn(integral_constant<int, i>) for i = 0 .. N-1, in order.
+template <int N, int I = 0, typename Fn>
+__device__ __forceinline__ void static_for(Fn&& fn) {
+  if constexpr (I < N) {
+    fn(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(static_cast<Fn&&>(fn));
+  }
+}
+
 template <int D, bool PREFIX>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
@@ -400,32 +422,101 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
           for (int qs = 0; qs < QB; ++qs) mask_tail(s0[qs], 0, hf, nvalid);
         }
         // Two regions: QK^T of block 1 with the weights of block 0, then PV of block 0
-        // with the weights of block 1. Each holds QB * D/16 MFMAs and about 48 QB
-        // vector instructions (per element: fma, exp, half a conversion, half a dot2).
-        // At d = 96 and 128 the regions are fenced and the vector work is spread
-        // evenly between the MFMAs (3% faster than the scheduler's own order); at
-        // d = 64 the unfenced interleave with LDS reads measured 1-2% better.
-        constexpr bool kFence = D != 64;
-        constexpr int kMfma = QB * (D / 16), kValuPerMfma = 768 / D;
-        if constexpr (kFence) __builtin_amdgcn_sched_barrier(0);
-        qk_block<D, QB>(sK[buf], qf, ka, 1, s1);
+        // with the weights of block 1. Each holds QB * D/16 MFMAs and 16 QB weights.
+        constexpr int kMfma = QB * (D / 16);
+        if constexpr (QB == 2) {
+          // Written as packets of one MFMA and an even share of the weight pairs, with
+          // a scheduling fence after each, so the vector work issues while the matrix
+          // core runs (1.5-2.5% faster at d = 64 and 96 than a scheduling hint per
+          // region). Operand fragments are read from LDS two packets before their
+          // first use, into three rotating registers.
+          constexpr int kPairs = QB * 8;
+          float mc[QB];
+          u32x4 pw[QB][2];
+          auto weights_share = [&](auto ic, const f32x16(&sb)[QB], float(&ls)[QB]) {
+            constexpr int i = decltype(ic)::value;
 #pragma unroll
-        for (int qs = 0; qs < QB; ++qs) l0[qs] = block_weights(s0[qs], c, m_ref[qs] * c, p0[qs]);
-        if constexpr (kFence) spread_valu_over_mfma<kMfma, kValuPerMfma>();
-        else interleave_mfma_valu<kMfma, 24 * QB>();
-        check_block(s0, p0, l0);
-        if (nvalid < kBlockK) {
+            for (int j = i * kPairs / kMfma; j < (i + 1) * kPairs / kMfma; ++j)
+              pair_weights(sb[j / 8], (j / 4) % 2, j % 4, c, mc[j / 8], pw[j / 8][(j / 4) % 2],
+                           ls[j / 8]);
+          };
+          auto start_weights = [&](float(&ls)[QB]) {
 #pragma unroll
-          for (int qs = 0; qs < QB; ++qs) mask_tail(s1[qs], 1, hf, nvalid);
+            for (int qs = 0; qs < QB; ++qs) {
+              mc[qs] = m_ref[qs] * c;
+              ls[qs] = 0.f;
+            }
+          };
+          auto finish_weights = [&](bf16x8(&p)[QB][2]) {
+#pragma unroll
+            for (int qs = 0; qs < QB; ++qs)
+#pragma unroll
+              for (int c2 = 0; c2 < 2; ++c2) p[qs][c2] = __builtin_bit_cast(bf16x8, pw[qs][c2]);
+          };
+
+          start_weights(l0);
+          {
+            const uint16_t* kb1 = sK[buf] + 32 * D;
+            bf16x8 kf[3];
+            kf[0] = as_bf16x8(load16(kb1 + ka.at[0]));
+            kf[1] = as_bf16x8(load16(kb1 + ka.at[1]));
+            __builtin_amdgcn_sched_barrier(0);
+            static_for<kMfma>([&](auto ic) {
+              constexpr int i = decltype(ic)::value, cc = i / QB, qs = i % QB;
+              if constexpr (qs == 0 && cc + 2 < D / 16)
+                kf[(cc + 2) % 3] = as_bf16x8(load16(kb1 + ka.at[cc + 2]));
+              s1[qs] = mfma32(kf[cc % 3], qf[qs][cc], cc == 0 ? f32x16{} : s1[qs]);
+              weights_share(ic, s0, l0);
+              __builtin_amdgcn_sched_barrier(0);
+            });
+          }
+          finish_weights(p0);
+          check_block(s0, p0, l0);
+          if (nvalid < kBlockK) {
+#pragma unroll
+            for (int qs = 0; qs < QB; ++qs) mask_tail(s1[qs], 1, hf, nvalid);
+          }
+          start_weights(l1);
+          {
+            constexpr int kMb = D / 32;  // fragment f of the block: chunk f / kMb, d-block f % kMb
+            bf16x8 vf[3];
+            vf[0] = vt_frag<D>(sV[buf], va, 0, 0);
+            vf[1] = vt_frag<D>(sV[buf], va, 1 % kMb, 1 / kMb);
+            __builtin_amdgcn_sched_barrier(0);
+            static_for<kMfma>([&](auto ic) {
+              constexpr int i = decltype(ic)::value, f = i / QB, qs = i % QB;
+              if constexpr (qs == 0 && f + 2 < 2 * kMb)
+                vf[(f + 2) % 3] = vt_frag<D>(sV[buf], va, (f + 2) % kMb, (f + 2) / kMb);
+              o[qs][f % kMb] = mfma32(vf[f % 3], p0[qs][f / kMb], o[qs][f % kMb]);
+              weights_share(ic, s1, l1);
+              __builtin_amdgcn_sched_barrier(0);
+            });
+          }
+          finish_weights(p1);
+        } else {
+          // One column block (d = 128): the regions are fenced and the vector work is
+          // spread evenly between the MFMAs by a scheduling hint (about 48 vector
+          // instructions per block: fma, exp, half a conversion, half a dot2 per
+          // element).
+          constexpr int kValuPerMfma = 768 / D;
+          __builtin_amdgcn_sched_barrier(0);
+          qk_block<D, QB>(sK[buf], qf, ka, 1, s1);
+#pragma unroll
+          for (int qs = 0; qs < QB; ++qs) l0[qs] = block_weights(s0[qs], c, m_ref[qs] * c, p0[qs]);
+          spread_valu_over_mfma<kMfma, kValuPerMfma>();
+          check_block(s0, p0, l0);
+          if (nvalid < kBlockK) {
+#pragma unroll
+            for (int qs = 0; qs < QB; ++qs) mask_tail(s1[qs], 1, hf, nvalid);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          pv_block<D, QB>(sV[buf], p0, va, 0, o);
+#pragma unroll
+          for (int qs = 0; qs < QB; ++qs) l1[qs] = block_weights(s1[qs], c, m_ref[qs] * c, p1[qs]);
+          spread_valu_over_mfma<kMfma, kValuPerMfma>();
         }
-        if constexpr (kFence) __builtin_amdgcn_sched_barrier(0);
-        pv_block<D, QB>(sV[buf], p0, va, 0, o);
-#pragma unroll
-        for (int qs = 0; qs < QB; ++qs) l1[qs] = block_weights(s1[qs], c, m_ref[qs] * c, p1[qs]);
-        if constexpr (kFence) spread_valu_over_mfma<kMfma, kValuPerMfma>();
-        else interleave_mfma_valu<kMfma, 24 * QB>();
         check_block(s1, p1, l1);
-        if constexpr (kFence) __builtin_amdgcn_sched_barrier(0);
+        if constexpr (QB != 2) __builtin_amdgcn_sched_barrier(0);
         pv_block<D, QB>(sV[buf], p1, va, 1, o);
       }
       cur = nxt;

@@ -17,6 +17,7 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -148,20 +149,6 @@ __device__ __forceinline__ void wait_tile_loads() { asm volatile("s_waitcnt vmcn
 __device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
   return __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) uint16_t*)p));
-}
-
-// Scheduling hint for a region holding N_MFMA matrix instructions (with their LDS
-// fragment reads) and about N_VALU vector instructions that do not depend on
-// them: each MFMA is followed by a share of the VALU work and one LDS read.
-template <int N_MFMA, int N_VALU>
-__device__ __forceinline__ void interleave_mfma_valu() {
-  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
-#pragma unroll
-  for (int i = 0; i < N_MFMA; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x002, (N_VALU + N_MFMA - 1) / N_MFMA, 0);  // VALU
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                        // DS read
-  }
 }
 
 // Scheduling hint for a region holding N_MFMA matrix instructions and about
