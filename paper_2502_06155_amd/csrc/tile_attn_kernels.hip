@@ -427,12 +427,15 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
         if constexpr (QB == 2) {
           // Written as packets of one MFMA and an even share of the weight pairs, with
           // a scheduling fence after each, so the vector work issues while the matrix
-          // core runs (1.5-2.5% faster at d = 64 and 96 than a scheduling hint per
+          // core runs (about 2% faster at d = 64 and 96 than a scheduling hint per
           // region). Operand fragments are read from LDS two packets before their
-          // first use, into three rotating registers.
+          // first use, into three rotating registers, and the last packets of a region
+          // already read the first two V^T fragments of the next PV region (1% more).
           constexpr int kPairs = QB * 8;
+          constexpr int kMb = D / 32;  // V^T fragment f of a block: chunk f / kMb, d-block f % kMb
           float mc[QB];
           u32x4 pw[QB][2];
+          bf16x8 vn[2];  // the first two V^T fragments of the next PV region
           auto weights_share = [&](auto ic, const f32x16(&sb)[QB], float(&ls)[QB]) {
             constexpr int i = decltype(ic)::value;
 #pragma unroll
@@ -453,6 +456,23 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
 #pragma unroll
               for (int c2 = 0; c2 < 2; ++c2) p[qs][c2] = __builtin_bit_cast(bf16x8, pw[qs][c2]);
           };
+          // O^T += V^T * P^T over block kb, one packet per MFMA; extra(ic) adds the
+          // packet's vector work. Block 0's packets read block 1's first fragments.
+          auto pv_packets = [&](auto kbc, const bf16x8(&p)[QB][2], auto&& extra) {
+            constexpr int kb = decltype(kbc)::value;
+            bf16x8 vf[3];
+            vf[0] = vn[0];
+            vf[1] = vn[1];
+            static_for<kMfma>([&](auto ic) {
+              constexpr int i = decltype(ic)::value, f = i / QB, qs = i % QB, g = f + 2 - 2 * kMb;
+              if constexpr (qs == 0 && g < 0)
+                vf[(f + 2) % 3] = vt_frag<D>(sV[buf], va, (f + 2) % kMb, 2 * kb + (f + 2) / kMb);
+              if constexpr (kb == 0 && qs == 0 && g >= 0) vn[g] = vt_frag<D>(sV[buf], va, g % kMb, 2 + g / kMb);
+              o[qs][f % kMb] = mfma32(vf[f % 3], p[qs][f / kMb], o[qs][f % kMb]);
+              extra(ic);
+              __builtin_amdgcn_sched_barrier(0);
+            });
+          };
 
           start_weights(l0);
           {
@@ -462,9 +482,9 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
             kf[1] = as_bf16x8(load16(kb1 + ka.at[1]));
             __builtin_amdgcn_sched_barrier(0);
             static_for<kMfma>([&](auto ic) {
-              constexpr int i = decltype(ic)::value, cc = i / QB, qs = i % QB;
-              if constexpr (qs == 0 && cc + 2 < D / 16)
-                kf[(cc + 2) % 3] = as_bf16x8(load16(kb1 + ka.at[cc + 2]));
+              constexpr int i = decltype(ic)::value, cc = i / QB, qs = i % QB, g = cc + 2 - D / 16;
+              if constexpr (qs == 0 && g < 0) kf[(cc + 2) % 3] = as_bf16x8(load16(kb1 + ka.at[cc + 2]));
+              if constexpr (qs == 0 && g >= 0) vn[g] = vt_frag<D>(sV[buf], va, g % kMb, g / kMb);
               s1[qs] = mfma32(kf[cc % 3], qf[qs][cc], cc == 0 ? f32x16{} : s1[qs]);
               weights_share(ic, s0, l0);
               __builtin_amdgcn_sched_barrier(0);
@@ -477,22 +497,10 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
             for (int qs = 0; qs < QB; ++qs) mask_tail(s1[qs], 1, hf, nvalid);
           }
           start_weights(l1);
-          {
-            constexpr int kMb = D / 32;  // fragment f of the block: chunk f / kMb, d-block f % kMb
-            bf16x8 vf[3];
-            vf[0] = vt_frag<D>(sV[buf], va, 0, 0);
-            vf[1] = vt_frag<D>(sV[buf], va, 1 % kMb, 1 / kMb);
-            __builtin_amdgcn_sched_barrier(0);
-            static_for<kMfma>([&](auto ic) {
-              constexpr int i = decltype(ic)::value, f = i / QB, qs = i % QB;
-              if constexpr (qs == 0 && f + 2 < 2 * kMb)
-                vf[(f + 2) % 3] = vt_frag<D>(sV[buf], va, (f + 2) % kMb, (f + 2) / kMb);
-              o[qs][f % kMb] = mfma32(vf[f % 3], p0[qs][f / kMb], o[qs][f % kMb]);
-              weights_share(ic, s1, l1);
-              __builtin_amdgcn_sched_barrier(0);
-            });
-          }
+          pv_packets(std::integral_constant<int, 0>{}, p0, [&](auto ic) { weights_share(ic, s1, l1); });
           finish_weights(p1);
+          check_block(s1, p1, l1);
+          pv_packets(std::integral_constant<int, 1>{}, p1, [](auto) {});
         } else {
           // One column block (d = 128): the regions are fenced and the vector work is
           // spread evenly between the MFMAs by a scheduling hint (about 48 vector
@@ -514,10 +522,10 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
 #pragma unroll
           for (int qs = 0; qs < QB; ++qs) l1[qs] = block_weights(s1[qs], c, m_ref[qs] * c, p1[qs]);
           spread_valu_over_mfma<kMfma, kValuPerMfma>();
+          check_block(s1, p1, l1);
+          __builtin_amdgcn_sched_barrier(0);
+          pv_block<D, QB>(sV[buf], p1, va, 1, o);
         }
-        check_block(s1, p1, l1);
-        if constexpr (QB != 2) __builtin_amdgcn_sched_barrier(0);
-        pv_block<D, QB>(sV[buf], p1, va, 1, o);
       }
       cur = nxt;
       nxt.advance(n_kept);
