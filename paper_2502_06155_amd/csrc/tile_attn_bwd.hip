@@ -123,10 +123,17 @@ struct DualLoader {
 // (the swizzle depends only on the low 4 bits of the row).
 template <int D>
 struct RowAddr {
-  int at[D / 16];
+  // At d = 96 the swizzle only permutes the low two bits of the piece index, so
+  // chunks cc and cc + 2 sit 4 pieces apart.
+  static constexpr int kN = D == 96 ? 2 : D / 16;
+  int at[kN];
   __device__ __forceinline__ void init(int n, int hf) {
 #pragma unroll
-    for (int cc = 0; cc < D / 16; ++cc) at[cc] = d_slot<D>(n, 2 * cc + hf);
+    for (int cc = 0; cc < kN; ++cc) at[cc] = d_slot<D>(n, 2 * cc + hf);
+  }
+  __device__ __forceinline__ int get(int cc) const {
+    if constexpr (D == 96) return at[cc & 1] + 32 * (cc >> 1);
+    else return at[cc];
   }
 };
 
@@ -135,22 +142,27 @@ struct RowAddr {
 // (hi), d = 32 mb + 16(g%2) + 4(j%4) .. +3. Chunk ch (16 rows) adds 16 ch * D.
 template <int D>
 struct TrAddr {
-  int lo[D / 32], hi[D / 32];
+  // At d = 96 the swizzle leaves the quad index 4 mb of a piece alone: d-block mb
+  // sits 32 mb elements further.
+  static constexpr int kN = D == 96 ? 1 : D / 32;
+  int lo[kN], hi[kN];
   __device__ __forceinline__ void init(int lane) {
     const int g = lane >> 4, j = lane & 15;
     const int r = 4 * (g >> 1) + (j >> 2);
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) {
+    for (int mb = 0; mb < kN; ++mb) {
       const int p = 4 * mb + 2 * (g & 1) + ((j >> 1) & 1);
       lo[mb] = d_slot<D>(r, p) + 4 * (j & 1);
       hi[mb] = d_slot<D>(r + 8, p) + 4 * (j & 1);
     }
   }
+  __device__ __forceinline__ int get_lo(int mb) const { return D == 96 ? lo[0] + 32 * mb : lo[mb]; }
+  __device__ __forceinline__ int get_hi(int mb) const { return D == 96 ? hi[0] + 32 * mb : hi[mb]; }
 };
 
 template <int D>
 __device__ __forceinline__ bf16x8 row_frag(const uint16_t* tile, const RowAddr<D>& ra, int rb, int cc) {
-  return as_bf16x8(load16(tile + rb * 32 * D + ra.at[cc]));
+  return as_bf16x8(load16(tile + rb * 32 * D + ra.get(cc)));
 }
 
 // 32 d-rows x 16 tile rows: the contraction index k of lane half h maps to tile
@@ -159,8 +171,8 @@ __device__ __forceinline__ bf16x8 row_frag(const uint16_t* tile, const RowAddr<D
 template <int D>
 __device__ __forceinline__ bf16x8 tr_frag(const uint16_t* tile, const TrAddr<D>& ta, int mb, int ch) {
   const uint16_t* p = tile + 16 * ch * D;
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + ta.lo[mb]));
-  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + ta.hi[mb]));
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + ta.get_lo(mb)));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + ta.get_hi(mb)));
   const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
   return as_bf16x8(u32x4{a[0], a[1], b[0], b[1]});
 }
@@ -412,6 +424,15 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
   }
 }
 
+// fn(integral_constant<int, i>) for i = 0 .. N-1, in order.
+template <int N, int I = 0, typename Fn>
+__device__ __forceinline__ void static_for(Fn&& fn) {
+  if constexpr (I < N) {
+    fn(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(static_cast<Fn&&>(fn));
+  }
+}
+
 // ---------------------------------------------------------------------------
 // dk/dv pass.
 template <int D, bool PREFIX, int MODE>
@@ -559,26 +580,115 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
       constexpr int buf = decltype(bufc)::value;
       if (t + 1 < n_tiles) load_tile(nxt, buf ^ 1);
       if (wave_active) {
-        // Program order: both halves' -delta reads, S, then dP (so the reads land
-        // while S forms), then half 0's P and dS and dV/dK update ahead of half 1's
-        // P and dS; the compiler interleaves them (fencing the phases, as in the dq
-        // pass, measured 4% slower here).
-        f32x16 s0, dp0, s1, dp1;
-        bf16x8 pb0[2], db0[2], pb1[2], db1[2];
-        if constexpr (kWantDk) {
-          dp_start(buf, 0, dp0);
-          dp_start(buf, 1, dp1);
+        if constexpr (MODE == kDkDv) {
+          // One stream of 8 D/16 MFMAs, each in a fenced packet with its share of the
+          // vector work; the operand fragment of MFMA i is read from LDS at packet
+          // i - 2 into one of three rotating registers, so no MFMA waits on a read
+          // issued just before it (3.5% faster than leaving the order to the
+          // compiler). Stream: S and dP of half 0, S and dP of half 1 (with half 0's
+          // P and dS forming), the dV/dK update of half 0 (with half 1's P and dS
+          // forming), the update of half 1.
+          constexpr int kC = Sh::kChunks, kMb = Sh::kDBlocks;
+          constexpr int kHalf = 2 * kC;             // S + dP MFMAs of a half
+          constexpr int kAcc = 4 * kMb;             // dV + dK MFMAs of a half
+          constexpr int kN = 2 * kHalf + 2 * kAcc;  // the whole stream
+          f32x16 sc[2], dp[2];
+          bf16x8 pb[2][2], db[2][2];
+          f32x4 l4[2][4];  // lse2 of this lane's 16 queries of each half, 4 at a time
+          auto frag = [&](auto ic) -> bf16x8 {
+            constexpr int i = decltype(ic)::value;
+            if constexpr (i < 2 * kHalf) {
+              constexpr int h = i / kHalf, r = i % kHalf;
+              if constexpr (r < kC) return row_frag<D>(sQ[buf], ra, h, r);
+              else return row_frag<D>(sG[buf], ra, h, r - kC);
+            } else {
+              constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
+              constexpr int c2 = r / (2 * kMb), mb = (r % (2 * kMb)) / 2, is_dk = r % 2;
+              return tr_frag<D>(is_dk ? sQ[buf] : sG[buf], ta, mb, 2 * h + c2);
+            }
+          };
+          auto mfma = [&](auto ic, const bf16x8& f) {
+            constexpr int i = decltype(ic)::value;
+            if constexpr (i < 2 * kHalf) {
+              constexpr int h = i / kHalf, r = i % kHalf;
+              if constexpr (r < kC) sc[h] = mfma32(f, kf[r], r == 0 ? f32x16{} : sc[h]);
+              else dp[h] = mfma32(f, vf[r - kC], dp[h]);
+            } else {
+              constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
+              constexpr int c2 = r / (2 * kMb), mb = (r % (2 * kMb)) / 2, is_dk = r % 2;
+              if constexpr (is_dk) dk[mb] = mfma32(f, db[h][c2], dk[mb]);
+              else dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
+            }
+          };
+          // Vector work of packet i: LDS reads of -delta (dP starts) and lse2 ahead of
+          // their use, and P, dS of half 0 over the second half's S/dP packets, of half
+          // 1 over half 0's update packets, 2 queries at a time.
+          auto side = [&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            if constexpr (i == 0 || i == kHalf) dp_start(buf, i / kHalf, dp[i / kHalf]);
+            // lse2 of queries 4 q4 .. 4 q4 + 3 (entries 4 q4 ..) of half hh, read two
+            // packets before the first packet whose share needs them.
+            static_for<8>([&](auto qc) {
+              constexpr int hh = decltype(qc)::value / 4, q4 = decltype(qc)::value % 4;
+              constexpr int st = hh == 0 ? kHalf : 2 * kHalf, pk = hh == 0 ? kHalf : kAcc;
+              constexpr int at = st + ((2 * q4 + 1) * pk + 7) / 8 - 1 - 2;
+              if constexpr (at == i)
+                l4[hh][q4] = *reinterpret_cast<const f32x4*>(&sL[buf][32 * hh + 16 * (q4 / 2) + 8 * (q4 % 2) + 4 * hf]);
+            });
+            constexpr int h = i < kHalf ? -1 : (i < 2 * kHalf ? 0 : (i < 2 * kHalf + kAcc ? 1 : -1));
+            if constexpr (h >= 0) {
+              constexpr int k = h == 0 ? i - kHalf : i - 2 * kHalf;  // packet within the share
+              constexpr int kPk = h == 0 ? kHalf : kAcc;
+#pragma unroll
+              for (int u = k * 8 / kPk; u < (k + 1) * 8 / kPk; ++u) {
+                // queries e, e+1 of the half: entry e = 8 c2 + 4 uu + j
+                const int e = 2 * u, c2 = e / 8, uu = (e % 8) / 4, j = e % 4;
+                const float p0 = prob(sc[h][e], a.c, l4[h][2 * c2 + uu][j]);
+                const float p1 = prob(sc[h][e + 1], a.c, l4[h][2 * c2 + uu][j + 1]);
+                const f32x2 pp = {p0, p1}, dd = {p0 * dp[h][e], p1 * dp[h][e + 1]};
+                const bf16x2 pq = __builtin_convertvector(pp, bf16x2);
+                const bf16x2 dq = __builtin_convertvector(dd, bf16x2);
+                u32x4 pw = __builtin_bit_cast(u32x4, pb[h][c2]), dw = __builtin_bit_cast(u32x4, db[h][c2]);
+                pw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, pq);
+                dw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, dq);
+                pb[h][c2] = __builtin_bit_cast(bf16x8, pw);
+                db[h][c2] = __builtin_bit_cast(bf16x8, dw);
+              }
+            }
+          };
+          bf16x8 fr[3];
+          fr[0] = frag(std::integral_constant<int, 0>{});
+          fr[1] = frag(std::integral_constant<int, 1>{});
+          __builtin_amdgcn_sched_barrier(0);
+          static_for<kN>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            if constexpr (i + 2 < kN) fr[(i + 2) % 3] = frag(std::integral_constant<int, i + 2>{});
+            mfma(ic, fr[i % 3]);
+            side(ic);
+            __builtin_amdgcn_sched_barrier(0);
+          });
+        } else {
+          // One of the two passes at d = 128: both halves' -delta reads, S, then dP
+          // (so the reads land while S forms), then half 0's P and dS and update
+          // ahead of half 1's; the compiler interleaves them (fencing the phases, as
+          // in the dq pass, measured 4% slower here).
+          f32x16 s0, dp0, s1, dp1;
+          bf16x8 pb0[2], db0[2], pb1[2], db1[2];
+          if constexpr (kWantDk) {
+            dp_start(buf, 0, dp0);
+            dp_start(buf, 1, dp1);
+          }
+          s_chain(buf, 0, s0);
+          s_chain(buf, 1, s1);
+          if constexpr (kWantDk) {
+            dp_chain(buf, 0, dp0);
+            dp_chain(buf, 1, dp1);
+          }
+          grads(buf, 0, s0, dp0, pb0, db0);
+          accumulate(buf, 0, pb0, db0);
+          grads(buf, 1, s1, dp1, pb1, db1);
+          accumulate(buf, 1, pb1, db1);
         }
-        s_chain(buf, 0, s0);
-        s_chain(buf, 1, s1);
-        if constexpr (kWantDk) {
-          dp_chain(buf, 0, dp0);
-          dp_chain(buf, 1, dp1);
-        }
-        grads(buf, 0, s0, dp0, pb0, db0);
-        accumulate(buf, 0, pb0, db0);
-        grads(buf, 1, s1, dp1, pb1, db1);
-        accumulate(buf, 1, pb1, db1);
       }
       cur = nxt;
       nxt.advance(n_keep);
