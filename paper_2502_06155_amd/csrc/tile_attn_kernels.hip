@@ -542,10 +542,16 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   // a split frame stores O/l in fp32 and its base-2 log-sum-exp
   // log2(sum_t 2^(c s_t)) = c m_ref + log2(l) for the merge. 4 consecutive d per
   // access.
+  // The lane's rows are derived again from a lane id read here, so that nothing
+  // lane-dependent from before the tile loop has to stay live across it.
+  int lane_e;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane_e));
+  const int hf_e = lane_e >> 5;
+  const int qrow0_e = qb * kBlockQ + wave * kWaveQ + (lane_e & 31);
 #pragma unroll
   for (int qs = 0; qs < QB; ++qs) {
     const float l_tot = pair_sum(l_run[qs]);
-    const int qrow = qrow0 + 32 * qs;
+    const int qrow = qrow0_e + 32 * qs;
     if (qrow < seg_len) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       if (slot < 0) {
@@ -557,9 +563,9 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
             f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
                        o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
             const bf16x4 y = __builtin_convertvector(x, bf16x4);
-            *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf) = __builtin_bit_cast(u32x2, y);
+            *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf_e) = __builtin_bit_cast(u32x2, y);
           }
-        if (lse && hf == 0)
+        if (lse && hf_e == 0)
           lse[(size_t)bh * head_rows + seg0 + qrow] =
               l_tot > 0.f ? (m_ref[qs] * c + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f
                           : -INFINITY;
@@ -574,9 +580,9 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
           for (int i = 0; i < 4; ++i) {
             const f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
                              o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
-            *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * i + 4 * hf) = x;
+            *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * i + 4 * hf_e) = x;
           }
-        if (hf == 0) ws_lse[prow] = m_ref[qs] * c + __builtin_amdgcn_logf(l_tot);
+        if (hf_e == 0) ws_lse[prow] = m_ref[qs] * c + __builtin_amdgcn_logf(l_tot);
       }
     }
   }
