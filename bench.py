@@ -84,22 +84,28 @@ def paper_stat(per_call):
     return float(np.median(a)), float(band.mean() if band.size else a.mean())
 
 
-def traffic_from_profile(which: str = "fwd"):
-    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
-    counter summary (FETCH_SIZE and WRITE_SIZE, each calibrated on a plain copy of
-    known size), or None when the summary was taken on other kernel sources."""
+def profile_record(which: str = "fwd", key: str = "hbm_bytes_per_launch"):
+    """One per-launch figure of the committed rocprofv3 counter summary, or None when
+    the summary was taken on other kernel sources. hbm_bytes_per_launch: HBM bytes
+    (FETCH_SIZE and WRITE_SIZE, each calibrated on a plain copy of known size);
+    mfma_bf16_flop_per_launch: SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP per op."""
     if not os.path.exists(PROFILE_MD[which]):
         return None
     rec = {}
     with open(PROFILE_MD[which]) as f:
         for line in f:
             if ":" in line and not line.startswith(("|", "#", " ", "`")):
-                key, _, val = line.partition(":")
-                rec[key.strip()] = val.strip()
+                k, _, val = line.partition(":")
+                rec[k.strip()] = val.strip()
     sha = hashlib.sha256(b"".join(open(p, "rb").read() for p in KERNEL_SRCS[which])).hexdigest()
-    if rec.get("kernel_sha256") != sha or "hbm_bytes_per_launch" not in rec:
+    if rec.get("kernel_sha256") != sha or key not in rec:
         return None
-    return float(rec["hbm_bytes_per_launch"])
+    return float(rec[key])
+
+
+def traffic_from_profile(which: str = "fwd"):
+    """HBM bytes per launch of the dominant kernel(s), or None (see profile_record)."""
+    return profile_record(which, "hbm_bytes_per_launch")
 
 
 def cpu_model() -> str:
@@ -451,6 +457,14 @@ def main():
         "cpu_baseline": cpu,
         "gemm_reference": gemm,
     }
+    # Matrix work the counters saw (padding included) over the same measured time.
+    mfma_flop = profile_record(which, "mfma_bf16_flop_per_launch")
+    if mfma_flop is not None:
+        ctf = mfma_flop / (np.mean(per) * 1e-3) / 1e12
+        line["mfma_counter"] = {"flop_per_launch": mfma_flop, "tflops": ctf,
+                                "frac": ctf / PEAK_BF16_TFLOPS,
+                                "source": "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, "
+                                          + os.path.relpath(PROFILE_MD[which], ROOT)}
     line.update(extra)
     print(json.dumps(line), flush=True)
 
