@@ -38,6 +38,13 @@
  *     its workspace freed and growing never waits for the stream. Later calls
  *     that fit allocate nothing and do not synchronise, so a warmed-up call can
  *     be captured in a HIP graph.
+ *   - The workspace is found by the stream handle: calls on one stream share it
+ *     in stream order, calls on different live streams never share one. Two
+ *     cases do share it with work that may still run, so avoid them: a stream
+ *     destroyed with calls still pending whose handle a new stream then receives
+ *     (synchronise a stream before destroying it), and a captured graph replayed
+ *     on another stream while calls run on the stream it was captured on (the
+ *     graph holds that stream's workspace).
  */
 #ifndef TILE_ATTN_H
 #define TILE_ATTN_H
