@@ -274,42 +274,43 @@ __device__ __forceinline__ void static_for(Fn&& fn) {
   }
 }
 
-template <int D, bool PREFIX>
-__global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
-    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
-    const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int H,
-    int F, int T, int P, int nqb, uint32_t n_wg, float* __restrict__ ws_o,
-    float* __restrict__ ws_lse, float* __restrict__ lse, float c, uint32_t qflip, uint32_t qmask) {
+// One workgroup's work item, decoded: the (batch, head) slabs, the query segment
+// and its query block, and the kept list.
+struct FwdItem {
+  const uint16_t* Qh;
+  const uint16_t* Kh;
+  const uint16_t* Vh;
+  uint16_t* Oh;
+  const int32_t* cols;
+  size_t head_rows;
+  uint32_t b, bh, per_b, n_wg;
+  int frame, kbeg, n_kept, slot, qb, seg0, seg_len;
+};
+
+// The rows of one workgroup with QB 32-query column blocks per wave. The grid's
+// query blocks hold fwd_rows_per_wg<D>() rows whatever QB is: a block at the end of
+// a segment with at most 32 valid rows per wave runs with QB = 1, so no wave computes
+// a column block that lies wholly past the segment end.
+template <int D, bool PREFIX, int QB>
+__device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>& lay,
+                                         uint16_t (&sK)[2][Shape<D>::kTileElems],
+                                         uint16_t (&sV)[2][Shape<D>::kTileElems],
+                                         float* __restrict__ ws_o, float* __restrict__ ws_lse,
+                                         float* __restrict__ lse, float c, uint32_t qflip,
+                                         uint32_t qmask) {
   using Sh = Shape<D>;
-  constexpr int QB = fwd_q_blocks<D>();
   constexpr int kWaveQ = 32 * QB;
   constexpr int kBlockQ = fwd_rows_per_wg<D>();
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
-
-  const uint32_t work = xcd_remap(blockIdx.x, n_wg);
-  const uint32_t per_b = (uint32_t)n_items * (uint32_t)nqb;
-  const uint32_t b = work / per_b;
-  const uint32_t rem = work - b * per_b;
-  const int32_t* item = items + 5 * (rem / nqb);
-  const uint32_t bh = b * (uint32_t)H + (uint32_t)item[0];
-  const int frame = item[1];
-  const int kbeg = item[2];
-  const int n_kept = item[3];
-  const int slot = item[4];  // >= 0: a piece of a split frame, written as a partial
-  const int qb = (int)(rem % nqb);
-  const Layout<PREFIX> lay{F, T, P};
-  const int seg0 = lay.start(frame), seg_len = lay.len(frame);
-  // With a prefix the text segment is shorter than the grid's query blocks assume.
-  if (PREFIX && qb * kBlockQ >= seg_len) return;
-
-  const size_t head_rows = (size_t)P * PREFIX + (size_t)F * T;
-  const size_t head_elems = head_rows * D;
-  const uint16_t* Qh = Q + bh * head_elems;
-  const uint16_t* Kh = K + bh * head_elems;
-  const uint16_t* Vh = V + bh * head_elems;
-  uint16_t* Oh = O + bh * head_elems;
+  const uint16_t* Qh = it.Qh;
+  const uint16_t* Kh = it.Kh;
+  const uint16_t* Vh = it.Vh;
+  uint16_t* Oh = it.Oh;
+  const int32_t* cols = it.cols;
+  const size_t head_rows = it.head_rows;
+  const uint32_t b = it.b, bh = it.bh, per_b = it.per_b, n_wg = it.n_wg;
+  const int kbeg = it.kbeg, n_kept = it.n_kept, slot = it.slot, qb = it.qb;
+  const int seg0 = it.seg0, seg_len = it.seg_len;
+  [[maybe_unused]] const int F = lay.F, T = lay.T, P = lay.P;
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
@@ -586,6 +587,57 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
       }
     }
   }
+}
+
+template <int D, bool PREFIX>
+__global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
+    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+    const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
+    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int H,
+    int F, int T, int P, int nqb, uint32_t n_wg, float* __restrict__ ws_o,
+    float* __restrict__ ws_lse, float* __restrict__ lse, float c, uint32_t qflip, uint32_t qmask) {
+  using Sh = Shape<D>;
+  constexpr int kBlockQ = fwd_rows_per_wg<D>();
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
+
+  FwdItem it;
+  const uint32_t work = xcd_remap(blockIdx.x, n_wg);
+  it.n_wg = n_wg;
+  it.per_b = (uint32_t)n_items * (uint32_t)nqb;
+  it.b = work / it.per_b;
+  const uint32_t rem = work - it.b * it.per_b;
+  const int32_t* item = items + 5 * (rem / nqb);
+  it.bh = it.b * (uint32_t)H + (uint32_t)item[0];
+  it.frame = item[1];
+  it.kbeg = item[2];
+  it.n_kept = item[3];
+  it.slot = item[4];  // >= 0: a piece of a split frame, written as a partial
+  it.qb = (int)(rem % nqb);
+  it.cols = cols;
+  const Layout<PREFIX> lay{F, T, P};
+  it.seg0 = lay.start(it.frame);
+  it.seg_len = lay.len(it.frame);
+  // With a prefix the text segment is shorter than the grid's query blocks assume.
+  if (PREFIX && it.qb * kBlockQ >= it.seg_len) return;
+
+  it.head_rows = (size_t)P * PREFIX + (size_t)F * T;
+  const size_t head_elems = it.head_rows * D;
+  it.Qh = Q + it.bh * head_elems;
+  it.Kh = K + it.bh * head_elems;
+  it.Vh = V + it.bh * head_elems;
+  it.Oh = O + it.bh * head_elems;
+
+  // A query block at the end of a segment with at most 32 valid rows per wave runs with
+  // one column block per wave. Only at d = 64: at d = 96 the second instance of the
+  // tile loop makes the register allocator spill the main one.
+  if constexpr (fwd_q_blocks<D>() == 2 && D == 64) {
+    if (it.seg_len - it.qb * kBlockQ <= kWaves * 32) {
+      fwd_rows<D, PREFIX, 1>(it, lay, sK, sV, ws_o, ws_lse, lse, c, qflip, qmask);
+      return;
+    }
+  }
+  fwd_rows<D, PREFIX, fwd_q_blocks<D>()>(it, lay, sK, sV, ws_o, ws_lse, lse, c, qflip, qmask);
 }
 
 // Combines the pieces of split query frames (or of the split text segment of the
