@@ -8,7 +8,9 @@
 // Work decomposition
 //   One workgroup = 4 waves = 256 query rows of one (batch, head, query frame);
 //   each wave owns 64 rows as two 32-query column blocks (128 rows and one block
-//   at d = 128, see fwd_q_blocks). Query blocks are frame aligned, so every row of
+//   at d = 128, see fwd_q_blocks; at d = 64 a block at the end of a frame with at
+//   most 32 valid rows per wave also runs one column block per wave, see
+//   fwd_rows). Query blocks are frame aligned, so every row of
 //   a workgroup shares one kept list. With a text prefix (the MM-DiT form) the text
 //   is one more segment, see Layout. Workgroup ids are
 //   remapped so that each XCD (8 per MI355X, each with its own L2) receives a
@@ -288,9 +290,9 @@ struct FwdItem {
 };
 
 // The rows of one workgroup with QB 32-query column blocks per wave. The grid's
-// query blocks hold fwd_rows_per_wg<D>() rows whatever QB is: a block at the end of
-// a segment with at most 32 valid rows per wave runs with QB = 1, so no wave computes
-// a column block that lies wholly past the segment end.
+// query blocks hold fwd_rows_per_wg<D>() rows whatever QB is: at d = 64 a block at the
+// end of a segment with at most 32 valid rows per wave runs with QB = 1, so no wave
+// computes a column block that lies wholly past the segment end.
 template <int D, bool PREFIX, int QB>
 __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>& lay,
                                          uint16_t (&sK)[2][Shape<D>::kTileElems],
