@@ -243,6 +243,33 @@ def test_last_query_block_with_idle_waves():
         assert_parity(got[0, h, s], ref, f"last-block-h{h}")
 
 
+def test_d64_tail_blocks_full_size():
+    """At d = 64 a frame's last query block whose rows fit 32 per wave (16 rows at
+    T = 3600) runs one 32-row column block per wave; every row of the last blocks of
+    all frames is compared, at a head count that fills the GPU."""
+    B, H, F, T, d = 1, 24, 3, 3600, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=22)
+    mask = om.tile_mask(F, 1, "col")
+    got = run_gpu(qb, kb, vb, mask, T, d ** -0.5)
+    rows = np.arange(T - 144, T)
+    for h in (0, 11, 23):
+        s = np.concatenate([f * T + rows for f in range(F)])
+        ref = oa.attention_rows(qb, kb, vb, mask, T, d ** -0.5, np.zeros_like(s), np.full_like(s, h), s)
+        assert_parity(got[0, h, s], ref, f"d64-last-block-h{h}")
+
+
+@pytest.mark.parametrize("T", [272, 356])
+def test_d64_tail_blocks_of_split_frames(T):
+    """d = 64 tail blocks (16 or 100 valid rows after a full 256-row block) in the
+    pieces of split heavy frames, which write fp32 partials from the one-column-block
+    epilogue before the merge; every row is compared with the oracle."""
+    B, H, F, d = 1, 2, 10, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=23)
+    mask = om.tile_mask(F, 1, "sym")
+    assert ta.tile_attn_plan(mask)[1] > 0
+    full_check(qb, kb, vb, mask, T, d ** -0.5, f"d64-tail-split-T{T}")
+
+
 # ---- split heavy query frames (partial results merged by log-sum-exp) -----------------
 
 @pytest.mark.parametrize("d", [64, 96, 128])
