@@ -29,8 +29,15 @@
  *     and nothing is enqueued. A HIP failure returns TA_ERR_HIP; the detail is in
  *     tile_attn_last_error().
  *   - Thread-safe. The first call for a given mask (per device) uploads its
- *     work plan (tile_attn_plan) with a blocking allocation and copy. A mask
- *     whose plan splits heavy query frames also needs a workspace for the
+ *     work plan (tile_attn_plan) with a blocking allocation and copy. Device
+ *     copies of plans are cached, at most TA_PLAN_CACHE_ENTRIES of them (each
+ *     4 * (5 * items + kept entries + 4 * split frames) bytes; a gradient call
+ *     holds two: the mask's and its transpose's). Beyond that the least recently
+ *     used one is evicted; its memory is freed only once no call holds it and
+ *     events recorded after every call that used it have completed, so evicting
+ *     never waits for a stream. A plan used while its stream is being captured
+ *     into a graph is never evicted (the graph may replay at any later time). A
+ *     mask whose plan splits heavy query frames also needs a workspace for the
  *     partial results, n_slots * B * max(T, P) * (d + 1) * 4 bytes (n_slots
  *     counts the pieces of all heads), held per (device, stream). A call that
  *     needs more allocates a larger one (at least 1.5 times the size) and keeps
@@ -56,6 +63,7 @@ extern "C" {
 #endif
 
 #define TA_MAX_FRAMES 1024
+#define TA_PLAN_CACHE_ENTRIES 256
 
 typedef enum {
   TA_OK = 0,
@@ -235,6 +243,15 @@ int tile_attn_compact(const uint8_t* tile_mask, int F, int32_t* row_ptr,
  */
 int tile_attn_plan(const uint8_t* tile_mask, int F, int32_t* items, int cap, int* n_items,
                    int* n_slots);
+
+/*
+ * Occupancy of the plan cache (all devices): *live receives the number of cached
+ * plans (at most TA_PLAN_CACHE_ENTRIES, plus any held by calls in progress or pinned
+ * by graph capture), *retired the number of evicted plans whose memory waits for
+ * their last kernels to finish. Frees the retired plans whose work is done first.
+ * Host only; TA_ERR_NULL_PTR for a NULL argument.
+ */
+int tile_attn_plan_cache_stats(int* live, int* retired);
 
 /* Static text for a status code. */
 const char* tile_attn_status_string(int status);

@@ -20,4 +20,5 @@ from .api import (  # noqa: F401
     tile_attn_fwd_mmdit,
     tile_attn_make_mask,
     tile_attn_plan,
+    tile_attn_plan_cache_stats,
 )

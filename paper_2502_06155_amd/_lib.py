@@ -20,6 +20,7 @@ EXPORTS = (
     "tile_attn_make_mask",
     "tile_attn_compact",
     "tile_attn_plan",
+    "tile_attn_plan_cache_stats",
     "tile_attn_status_string",
     "tile_attn_last_error",
 )
@@ -68,6 +69,8 @@ def _load() -> ctypes.CDLL:
     lib.tile_attn_compact.restype = ci
     lib.tile_attn_plan.argtypes = [vp, ci, vp, ci, ctypes.POINTER(ci), ctypes.POINTER(ci)]
     lib.tile_attn_plan.restype = ci
+    lib.tile_attn_plan_cache_stats.argtypes = [ctypes.POINTER(ci), ctypes.POINTER(ci)]
+    lib.tile_attn_plan_cache_stats.restype = ci
     lib.tile_attn_status_string.argtypes = [ci]
     lib.tile_attn_status_string.restype = ctypes.c_char_p
     lib.tile_attn_last_error.argtypes = []

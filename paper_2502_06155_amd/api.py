@@ -157,6 +157,15 @@ def tile_attn_plan(tile_mask):
     return items[: 4 * n_items.value].reshape(-1, 4).copy(), n_slots.value
 
 
+def tile_attn_plan_cache_stats():
+    """(live, retired): cached device plans and evicted ones still waiting for their
+    kernels to finish (tile_attn_plan_cache_stats of the C ABI)."""
+    live, retired = ctypes.c_int(0), ctypes.c_int(0)
+    _check(lib.tile_attn_plan_cache_stats(ctypes.byref(live), ctypes.byref(retired)),
+           "tile_attn_plan_cache_stats")
+    return live.value, retired.value
+
+
 def _shape_of(q, T: int):
     if q.dim() != 4:
         raise ValueError("expected [B, H, S, d] tensors")
@@ -166,12 +175,20 @@ def _shape_of(q, T: int):
     return B, H, S // T, d
 
 
-def _check_tensors(*ts):
+def _check_tensors(q, *others):
+    """q, k, v, out of the torch wrappers: the same [B, H, S, d] shape, contiguous
+    bfloat16 on one GPU. Checked before anything is launched: the kernels read and
+    write B*H*S*d elements of every tensor."""
     import torch
 
-    for t in ts:
+    for t in others:
+        if tuple(t.shape) != tuple(q.shape):
+            raise ValueError(f"k, v and out must have q's shape {tuple(q.shape)}, got {tuple(t.shape)}")
+    for t in (q, *others):
         if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
             raise ValueError("tensors must be contiguous bfloat16 on a GPU")
+        if t.device != q.device:
+            raise ValueError(f"every tensor must be on q's device {q.device}, got {t.device}")
 
 
 def tile_attn(q, k, v, tile_mask, T: int, scale: float | None = None, out=None):

@@ -1,0 +1,58 @@
+// Host-side pieces shared by the C-ABI translation units: error reporting, argument
+// checks, the work plan in host and device form, and the enqueue of the forward
+// kernels for a given plan and partial-result buffer.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace ta {
+namespace host {
+
+// Records the detail for tile_attn_last_error() and returns status.
+int fail(int status, const std::string& detail);
+void clear_error();
+
+// Checks shared by every forward entry point (TA_OK or an error status with its
+// detail recorded); nothing touches the GPU.
+int check_args(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
+               int T, int d, float scale, int P = 0);
+bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb);
+
+// The work plans of all heads resident on one device: [items][cols][heavy] in int32
+// words, read by the kernels with scalar loads. Items are {head, frame, first kept
+// entry, count, slot} with cols and slots offset per head; heavy entries are
+// {head, frame, first slot, slots}.
+struct DeviceWorkList {
+  void* buffer = nullptr;
+  const int32_t* items = nullptr;
+  const int32_t* cols = nullptr;
+  const int32_t* heavy = nullptr;
+  int n_items = 0, n_heavy = 0, n_slots = 0;
+};
+
+// The same plan as host words, before upload: offsets of cols and heavy in words.
+struct HostWorkList {
+  std::vector<int32_t> words;
+  size_t off_cols = 0, off_heavy = 0;
+  int n_items = 0, n_heavy = 0, n_slots = 0;
+};
+
+// Plans H heads with n_masks masks (1: shared, H: one per head) of F segments; heavy
+// query frames are split into pieces when allow_split.
+HostWorkList build_work_list(const uint8_t* masks, int n_masks, int H, int F, bool allow_split);
+
+// The device view of hw's words placed at buf.
+DeviceWorkList place_work_list(const HostWorkList& hw, void* buf);
+
+// Enqueues the forward kernel (and the merge of split frames) on stream for a plan
+// already resident on the device; ws holds n_slots * B * max(T, P) * (d + 1) floats
+// (unused when the plan has no slots).
+int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
+                int T, int d, int P, const DeviceWorkList& plan, float* ws, float scale,
+                float* lse, void* stream);
+
+}  // namespace host
+}  // namespace ta

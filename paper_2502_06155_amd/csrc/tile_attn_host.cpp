@@ -1,6 +1,7 @@
 // C-ABI entry points: argument checks, the k:(F-k) mask builder, compaction of
 // the frame mask into a kept-tile list and a work plan (query frames with many
-// kept frames split into balanced pieces), a per-device cache of that plan, a
+// kept frames split into balanced pieces), a bounded cache of the device copies of
+// those plans, a
 // per-(device, stream) workspace for the partial results of split frames, and
 // dispatch of the gfx950 kernels on the caller's stream.
 #include "../../include/tile_attn.h"
@@ -20,8 +21,11 @@
 #include <vector>
 
 #include "launch.h"
+#include "host_internal.h"
+#include "plan_cache.h"
 
-namespace {
+namespace ta {
+namespace host {
 
 thread_local std::string g_last_error;
 
@@ -29,6 +33,8 @@ int fail(int status, const std::string& detail) {
   g_last_error = detail;
   return status;
 }
+
+void clear_error() { g_last_error.clear(); }
 
 void compact_host(const uint8_t* mask, int F, int32_t* row_ptr, uint16_t* cols,
                   uint16_t* order, int* nnz_out) {
@@ -98,76 +104,7 @@ WorkPlan plan_work(const uint8_t* mask, int F, bool allow_split) {
   return pl;
 }
 
-// The work plans of all heads resident on one device: [items][cols][heavy] in int32
-// words, read by the kernels with scalar loads. Items are {head, frame, first kept
-// entry, count, slot} with cols and slots offset per head; heavy entries are
-// {head, frame, first slot, slots}.
-struct DeviceWorkList {
-  void* buffer = nullptr;
-  const int32_t* items = nullptr;
-  const int32_t* cols = nullptr;
-  const int32_t* heavy = nullptr;
-  int n_items = 0, n_heavy = 0, n_slots = 0;
-};
-
-std::mutex g_cache_mutex;
-std::map<std::pair<int, std::string>, DeviceWorkList> g_cache;
-
-// Partial-result workspace of split frames, one per (device, stream) so that calls
-// on different streams never share it; replaced by a larger one on demand, every
-// buffer kept until process exit.
-struct Workspace {
-  void* ptr = nullptr;
-  size_t bytes = 0;
-  std::vector<void*> retired;
-};
-std::map<std::pair<int, void*>, Workspace> g_workspaces;
-
-// Largest workspace a call may use; masks that would need more are not split.
-constexpr size_t kMaxWorkspaceBytes = size_t(2) << 30;
-
-bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
-  auto x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
-  return x < y + nb && y < x + na;
-}
-
-int check_args(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
-               int T, int d, float scale, int P = 0) {
-  if (!q || !k || !v || !out) return fail(TA_ERR_NULL_PTR, "q, k, v and out must be non-NULL");
-  if (B < 1 || H < 1 || F < 1 || T < 1)
-    return fail(TA_ERR_BAD_SHAPE, "B, H, F and T must be >= 1");
-  if (P < 0) return fail(TA_ERR_BAD_SHAPE, "the text prefix length must be >= 0");
-  if (F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F exceeds TA_MAX_FRAMES");
-  if ((int64_t)F * T + P > INT32_MAX) return fail(TA_ERR_BAD_SHAPE, "P + F * T exceeds 2^31 - 1");
-  if (d != 64 && d != 96 && d != 128) return fail(TA_ERR_HEAD_DIM, "d must be 64, 96 or 128");
-  const int rows = ta::fwd_rows_per_workgroup(d) > 0 ? ta::fwd_rows_per_workgroup(d) : 256;
-  const int64_t nqb = (std::max(T, P) + rows - 1) / rows;
-  const int64_t n_wg = (int64_t)B * H * (F + (P > 0)) * nqb;
-  if (n_wg * ta::kThreads > (int64_t)UINT32_MAX)
-    return fail(TA_ERR_BAD_SHAPE, "B * H * F * ceil(T / 256) workgroups exceed the grid limit");
-  if (!std::isfinite(scale)) return fail(TA_ERR_BAD_SCALE, "scale must be finite");
-  for (const void* p : {q, k, v, (const void*)out})
-    if (reinterpret_cast<uintptr_t>(p) % 16)
-      return fail(TA_ERR_ALIGN, "q, k, v and out must be 16-byte aligned");
-  const size_t bytes = (size_t)B * H * ((size_t)F * T + P) * d * 2;
-  for (const void* p : {q, k, v})
-    if (ranges_overlap(out, bytes, p, bytes)) return fail(TA_ERR_OVERLAP, "out overlaps an input");
-  return TA_OK;
-}
-
-// Returns the device-resident work list for H heads with n_masks masks (1: shared,
-// H: one per head), split or not, uploading it on first use on device dev.
-int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_split, int dev,
-                  const DeviceWorkList** out) {
-  std::string key(reinterpret_cast<const char*>(masks), (size_t)n_masks * F * F);
-  key += allow_split ? "|s|" : "|u|";
-  key += std::to_string(H) + "|" + std::to_string(n_masks);
-  std::lock_guard<std::mutex> lock(g_cache_mutex);
-  auto it = g_cache.find({dev, key});
-  if (it != g_cache.end()) {
-    *out = &it->second;
-    return TA_OK;
-  }
+HostWorkList build_work_list(const uint8_t* masks, int n_masks, int H, int F, bool allow_split) {
   std::vector<int32_t> items, cols, heavy;
   int n_slots = 0;
   WorkPlan shared;
@@ -190,34 +127,184 @@ int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_sp
       heavy.insert(heavy.end(), {h, pl.heavy[i], pl.heavy[i + 1] + n_slots, pl.heavy[i + 2]});
     n_slots += pl.n_slots;
   }
-  std::vector<int32_t> words;
-  words.insert(words.end(), items.begin(), items.end());
-  const size_t off_cols = words.size();
-  words.insert(words.end(), cols.begin(), cols.end());
-  const size_t off_heavy = words.size();
-  words.insert(words.end(), heavy.begin(), heavy.end());
-  if (heavy.empty()) words.push_back(0);
-  const size_t total = words.size() * sizeof(int32_t);
+  HostWorkList hw;
+  hw.words.insert(hw.words.end(), items.begin(), items.end());
+  hw.off_cols = hw.words.size();
+  hw.words.insert(hw.words.end(), cols.begin(), cols.end());
+  hw.off_heavy = hw.words.size();
+  hw.words.insert(hw.words.end(), heavy.begin(), heavy.end());
+  if (heavy.empty()) hw.words.push_back(0);
+  hw.n_items = (int)(items.size() / 5);
+  hw.n_heavy = (int)(heavy.size() / 4);
+  hw.n_slots = n_slots;
+  return hw;
+}
+
+DeviceWorkList place_work_list(const HostWorkList& hw, void* buf) {
+  DeviceWorkList wl;
+  wl.buffer = buf;
+  wl.items = static_cast<const int32_t*>(buf);
+  wl.cols = static_cast<const int32_t*>(buf) + hw.off_cols;
+  wl.heavy = static_cast<const int32_t*>(buf) + hw.off_heavy;
+  wl.n_items = hw.n_items;
+  wl.n_heavy = hw.n_heavy;
+  wl.n_slots = hw.n_slots;
+  return wl;
+}
+
+// A cached plan: its device buffer and, per stream that enqueued work with it, an
+// event recorded after that work (stream order makes the latest one cover the
+// earlier ones on the same stream).
+struct CachedPlan {
+  DeviceWorkList wl;
+  int dev = 0;
+  std::vector<std::pair<void*, hipEvent_t>> uses;
+};
+
+struct HipPlanOps {
+  bool idle(CachedPlan& p) {
+    bool done = true;
+    for (auto& u : p.uses) done = done && hipEventQuery(u.second) != hipErrorNotReady;
+    (void)hipGetLastError();  // a pending event's status is not an error of the caller's
+    return done;
+  }
+  void release(CachedPlan& p) {
+    int cur = 0;
+    const bool restore = hipGetDevice(&cur) == hipSuccess && cur != p.dev;
+    if (restore) (void)hipSetDevice(p.dev);
+    (void)hipFree(p.wl.buffer);
+    for (auto& u : p.uses) (void)hipEventDestroy(u.second);
+    if (restore) (void)hipSetDevice(cur);
+    (void)hipGetLastError();
+  }
+};
+
+std::mutex g_cache_mutex;
+ta::PlanCache<CachedPlan, HipPlanOps> g_cache(TA_PLAN_CACHE_ENTRIES);
+
+// A plan acquired for one call: a copy of its device addresses, and the cache slot the
+// call holds until end_plan_use() (so no eviction frees it before the call's kernels are
+// enqueued and their completion can be tracked).
+struct PlanUse {
+  DeviceWorkList wl;
+  ta::PlanCache<CachedPlan, HipPlanOps>::Handle slot = nullptr;
+};
+
+// Returns the device-resident work list for H heads with n_masks masks (1: shared,
+// H: one per head), split or not, uploading it on first use on device dev.
+int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_split, int dev,
+                  PlanUse* out) {
+  std::string key(reinterpret_cast<const char*>(masks), (size_t)n_masks * F * F);
+  key += allow_split ? "|s|" : "|u|";
+  key += std::to_string(H) + "|" + std::to_string(n_masks) + "|" + std::to_string(F) + "|" +
+         std::to_string(dev);
+  std::lock_guard<std::mutex> lock(g_cache_mutex);
+  if (auto h = g_cache.acquire(key)) {
+    out->wl = h->value.wl;
+    out->slot = h;
+    return TA_OK;
+  }
+  const HostWorkList hw = build_work_list(masks, n_masks, H, F, allow_split);
+  const size_t total = hw.words.size() * sizeof(int32_t);
   void* buf = nullptr;
   hipError_t e = hipMalloc(&buf, total);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
-  e = hipMemcpy(buf, words.data(), total, hipMemcpyHostToDevice);
+  e = hipMemcpy(buf, hw.words.data(), total, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(buf);
     return fail(TA_ERR_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
   }
-  DeviceWorkList entry;
-  entry.buffer = buf;
-  entry.items = static_cast<const int32_t*>(buf);
-  entry.cols = static_cast<const int32_t*>(buf) + off_cols;
-  entry.heavy = static_cast<const int32_t*>(buf) + off_heavy;
-  entry.n_items = (int)(items.size() / 5);
-  entry.n_heavy = (int)(heavy.size() / 4);
-  entry.n_slots = n_slots;
-  auto res = g_cache.emplace(std::make_pair(dev, std::move(key)), entry);
-  *out = &res.first->second;
+  CachedPlan cp;
+  cp.wl = place_work_list(hw, buf);
+  cp.dev = dev;
+  auto h = g_cache.insert(std::move(key), std::move(cp));
+  out->wl = h->value.wl;
+  out->slot = h;
   return TA_OK;
 }
+
+// The call has enqueued every kernel that reads the plan on `stream` (or failed to):
+// record an event after them, or, when the stream is being captured into a graph that
+// may replay at any later time, keep the plan for the rest of the process.
+void end_plan_use(PlanUse& u, void* stream) {
+  if (!u.slot) return;
+  std::lock_guard<std::mutex> lock(g_cache_mutex);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+    (void)hipGetLastError();
+    g_cache.pin(u.slot);
+  } else {
+    auto& uses = u.slot->value.uses;
+    auto it = std::find_if(uses.begin(), uses.end(),
+                           [&](const std::pair<void*, hipEvent_t>& x) { return x.first == stream; });
+    hipEvent_t ev = nullptr;
+    if (it != uses.end()) {
+      ev = it->second;
+    } else if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess) {
+      uses.emplace_back(stream, ev);
+    } else {
+      ev = nullptr;
+    }
+    if (!ev || hipEventRecord(ev, s) != hipSuccess) {
+      (void)hipGetLastError();
+      g_cache.pin(u.slot);  // completion cannot be tracked: never free it
+    }
+  }
+  g_cache.release(u.slot);
+  u.slot = nullptr;
+}
+
+// Holds a plan for the duration of a call and ends its use on every return path.
+struct PlanGuard {
+  PlanUse use;
+  void* stream;
+  explicit PlanGuard(void* s) : stream(s) {}
+  ~PlanGuard() { end_plan_use(use, stream); }
+};
+
+// Partial-result workspace of split frames, one per (device, stream) so that calls
+// on different streams never share it; replaced by a larger one on demand, every
+// buffer kept until process exit.
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+  std::vector<void*> retired;
+};
+std::map<std::pair<int, void*>, Workspace> g_workspaces;
+
+// Largest workspace a call may use; masks that would need more are not split.
+constexpr size_t kMaxWorkspaceBytes = size_t(2) << 30;
+
+bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  auto x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+int check_args(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
+               int T, int d, float scale, int P) {
+  if (!q || !k || !v || !out) return fail(TA_ERR_NULL_PTR, "q, k, v and out must be non-NULL");
+  if (B < 1 || H < 1 || F < 1 || T < 1)
+    return fail(TA_ERR_BAD_SHAPE, "B, H, F and T must be >= 1");
+  if (P < 0) return fail(TA_ERR_BAD_SHAPE, "the text prefix length must be >= 0");
+  if (F > TA_MAX_FRAMES) return fail(TA_ERR_BAD_SHAPE, "F exceeds TA_MAX_FRAMES");
+  if ((int64_t)F * T + P > INT32_MAX) return fail(TA_ERR_BAD_SHAPE, "P + F * T exceeds 2^31 - 1");
+  if (d != 64 && d != 96 && d != 128) return fail(TA_ERR_HEAD_DIM, "d must be 64, 96 or 128");
+  const int rows = ta::fwd_rows_per_workgroup(d) > 0 ? ta::fwd_rows_per_workgroup(d) : 256;
+  const int64_t nqb = (std::max(T, P) + rows - 1) / rows;
+  const int64_t n_wg = (int64_t)B * H * (F + (P > 0)) * nqb;
+  if (n_wg * ta::kThreads > (int64_t)UINT32_MAX)
+    return fail(TA_ERR_BAD_SHAPE, "B * H * F * ceil(T / 256) workgroups exceed the grid limit");
+  if (!std::isfinite(scale)) return fail(TA_ERR_BAD_SCALE, "scale must be finite");
+  for (const void* p : {q, k, v, (const void*)out})
+    if (reinterpret_cast<uintptr_t>(p) % 16)
+      return fail(TA_ERR_ALIGN, "q, k, v and out must be 16-byte aligned");
+  const size_t bytes = (size_t)B * H * ((size_t)F * T + P) * d * 2;
+  for (const void* p : {q, k, v})
+    if (ranges_overlap(out, bytes, p, bytes)) return fail(TA_ERR_OVERLAP, "out overlaps an input");
+  return TA_OK;
+}
+
 
 // Workspace of at least `bytes` for (dev, stream). One that is too small is replaced
 // by a larger one (at least 1.5 times the old size, so replacements stay few) and
@@ -245,41 +332,13 @@ int workspace_for(int dev, void* stream, size_t bytes, void** out) {
   return TA_OK;
 }
 
-int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F, int T,
-            int d, const uint8_t* masks, int n_masks, float scale, float* lse, void* stream,
-            int P = 0) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
-  const int L = std::max(T, P);  // longest segment: rows per query-block grid column
+int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
+                int T, int d, int P, const DeviceWorkList& plan, float* ws, float scale,
+                float* lse, void* stream) {
+  const DeviceWorkList* wl = &plan;
+  const int L = std::max(T, P);
   const int64_t nqb = (L + ta::fwd_rows_per_workgroup(d) - 1) / ta::fwd_rows_per_workgroup(d);
-  // With a text prefix, plan F + 1 segments: video row i keeps its mask row plus the
-  // text (segment F); the text row keeps everything.
-  std::vector<uint8_t> aug;
-  int n_seg = F;
-  if (P > 0) {
-    n_seg = F + 1;
-    aug.assign((size_t)n_masks * n_seg * n_seg, 1);
-    for (int m = 0; m < n_masks; ++m)
-      for (int i = 0; i < F; ++i)
-        for (int j = 0; j < F; ++j)
-          aug[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * F + i) * F + j] ? 1 : 0;
-    masks = aug.data();
-  }
-  const DeviceWorkList* wl = nullptr;
-  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &wl);
-  if (st != TA_OK) return st;
-  const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
-  if ((size_t)wl->n_slots * B * L * (d + 1) * sizeof(float) > kMaxWorkspaceBytes ||
-      (int64_t)B * wl->n_items * nqb > max_wg) {
-    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &wl);  // the same rows, not split
-    if (st != TA_OK) return st;
-  }
-  void* ws = nullptr;
-  if (wl->n_slots > 0) {
-    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * L * (d + 1) * sizeof(float), &ws);
-    if (st != TA_OK) return st;
-  }
+  hipError_t e;
   ta::FwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -294,8 +353,8 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   a.items = wl->items;
   a.cols = wl->cols;
   a.n_items = wl->n_items;
-  a.ws_o = static_cast<float*>(ws);
-  a.ws_lse = ws ? static_cast<float*>(ws) + (size_t)wl->n_slots * B * L * d : nullptr;
+  a.ws_o = ws;
+  a.ws_lse = ws ? ws + (size_t)wl->n_slots * B * L * d : nullptr;
   a.lse = lse;
   // Logits are formed from |scale| (a negative scale flips the sign of q, which
   // is exact in bf16). scale == 0 zeroes q instead, so every logit is exactly 0
@@ -329,6 +388,48 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
     e = ta::launch_merge_partials(m, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
   }
+  return TA_OK;
+}
+
+int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F, int T,
+            int d, const uint8_t* masks, int n_masks, float scale, float* lse, void* stream,
+            int P = 0) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  const int L = std::max(T, P);  // longest segment: rows per query-block grid column
+  const int64_t nqb = (L + ta::fwd_rows_per_workgroup(d) - 1) / ta::fwd_rows_per_workgroup(d);
+  // With a text prefix, plan F + 1 segments: video row i keeps its mask row plus the
+  // text (segment F); the text row keeps everything.
+  std::vector<uint8_t> aug;
+  int n_seg = F;
+  if (P > 0) {
+    n_seg = F + 1;
+    aug.assign((size_t)n_masks * n_seg * n_seg, 1);
+    for (int m = 0; m < n_masks; ++m)
+      for (int i = 0; i < F; ++i)
+        for (int j = 0; j < F; ++j)
+          aug[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * F + i) * F + j] ? 1 : 0;
+    masks = aug.data();
+  }
+  PlanGuard plan(stream);
+  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &plan.use);
+  if (st != TA_OK) return st;
+  const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
+  if ((size_t)plan.use.wl.n_slots * B * L * (d + 1) * sizeof(float) > kMaxWorkspaceBytes ||
+      (int64_t)B * plan.use.wl.n_items * nqb > max_wg) {
+    end_plan_use(plan.use, stream);
+    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &plan.use);  // the same rows, not split
+    if (st != TA_OK) return st;
+  }
+  const DeviceWorkList* wl = &plan.use.wl;
+  void* ws = nullptr;
+  if (wl->n_slots > 0) {
+    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * L * (d + 1) * sizeof(float), &ws);
+    if (st != TA_OK) return st;
+  }
+  st = enqueue_fwd(q, k, v, out, B, H, F, T, d, P, *wl, static_cast<float*>(ws), scale, lse, stream);
+  if (st != TA_OK) return st;
   g_last_error.clear();
   return TA_OK;
 }
@@ -364,25 +465,30 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
           aug[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * F + i) * F + j] ? 1 : 0;
     masks = aug.data();
   }
-  const DeviceWorkList* wq = nullptr;
-  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &wq);
+  PlanGuard plan_q(stream), plan_k(stream);
+  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &plan_q.use);
   if (st != TA_OK) return st;
-  if ((size_t)wq->n_slots * part_row > kMaxWorkspaceBytes || (int64_t)B * wq->n_items * nqb > max_wg) {
-    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &wq);
+  if ((size_t)plan_q.use.wl.n_slots * part_row > kMaxWorkspaceBytes ||
+      (int64_t)B * plan_q.use.wl.n_items * nqb > max_wg) {
+    end_plan_use(plan_q.use, stream);
+    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &plan_q.use);
     if (st != TA_OK) return st;
   }
+  const DeviceWorkList* wq = &plan_q.use.wl;
   std::vector<uint8_t> mt((size_t)n_masks * n_seg * n_seg);
   for (int m = 0; m < n_masks; ++m)
     for (int i = 0; i < n_seg; ++i)
       for (int j = 0; j < n_seg; ++j)
         mt[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * n_seg + j) * n_seg + i];
-  const DeviceWorkList* wk = nullptr;
-  st = work_list_for(mt.data(), n_masks, H, n_seg, true, dev, &wk);
+  st = work_list_for(mt.data(), n_masks, H, n_seg, true, dev, &plan_k.use);
   if (st != TA_OK) return st;
-  if ((size_t)wk->n_slots * 2 * part_row > kMaxWorkspaceBytes || (int64_t)B * wk->n_items * nkb > max_wg) {
-    st = work_list_for(mt.data(), n_masks, H, n_seg, false, dev, &wk);
+  if ((size_t)plan_k.use.wl.n_slots * 2 * part_row > kMaxWorkspaceBytes ||
+      (int64_t)B * plan_k.use.wl.n_items * nkb > max_wg) {
+    end_plan_use(plan_k.use, stream);
+    st = work_list_for(mt.data(), n_masks, H, n_seg, false, dev, &plan_k.use);
     if (st != TA_OK) return st;
   }
+  const DeviceWorkList* wk = &plan_k.use.wl;
 
   const size_t rows = (size_t)B * H * ((size_t)F * T + P);
   const size_t bytes = rows * 2 * sizeof(float) + (size_t)wq->n_slots * part_row +
@@ -476,7 +582,10 @@ int run_bwd(const void* q, const void* k, const void* v, const void* out, const 
   return TA_OK;
 }
 
-}  // namespace
+}  // namespace host
+}  // namespace ta
+
+using namespace ta::host;
 
 extern "C" {
 
@@ -655,5 +764,14 @@ const char* tile_attn_status_string(int status) {
 }
 
 const char* tile_attn_last_error(void) { return g_last_error.c_str(); }
+
+int tile_attn_plan_cache_stats(int* live, int* retired) {
+  if (!live || !retired) return fail(TA_ERR_NULL_PTR, "live and retired must be non-NULL");
+  std::lock_guard<std::mutex> lock(g_cache_mutex);
+  g_cache.collect();
+  *live = (int)g_cache.size();
+  *retired = (int)g_cache.retired();
+  return TA_OK;
+}
 
 }  // extern "C"

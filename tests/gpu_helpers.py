@@ -67,3 +67,31 @@ def sample_rows(B, H, F, T, per_frame=4, heads=None, seed=0):
                     hs.append(h)
                     ss.append(f * T + r)
     return np.array(bs), np.array(hs), np.array(ss)
+
+
+# Inputs of the named workloads, drawn once per process: the 93-frame shapes take tens
+# of seconds of host time to draw and round, and several test modules use them.
+_WORKLOAD_INPUTS = {}
+
+
+def workload_inputs(name: str):
+    """(qb, kb, vb) bf16 bits of workloads.WORKLOADS[name] (its own seed and recipe)."""
+    import workloads
+
+    if name not in _WORKLOAD_INPUTS:
+        _WORKLOAD_INPUTS[name] = workloads.make_workload_qkv(workloads.WORKLOADS[name])
+    return _WORKLOAD_INPUTS[name]
+
+
+_GRADS = {}
+
+
+def upstream_grad(shape, seed: int):
+    """An N(0, 1) upstream gradient as bf16 bits from its own PCG64 stream, cached."""
+    import workloads
+
+    key = (tuple(shape), seed)
+    if key not in _GRADS:
+        rng = np.random.default_rng(seed)
+        _GRADS[key] = workloads.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    return _GRADS[key]

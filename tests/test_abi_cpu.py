@@ -239,3 +239,40 @@ def test_bwd_mmdit_argument_errors_before_any_gpu_call():
     assert call(dout=None) == 1
     assert call(dq=(1 << 13) + 4096) == 7  # dq overlaps q over P + F*T tokens
     assert call(dk=(9 << 13) - 4096) == 7  # dk overlaps dv
+
+
+def test_torch_wrappers_reject_mismatched_tensors_before_launch():
+    """The torch wrappers check k, v and out against q's shape before anything reaches
+    the library (on CPU tensors the shape check fires first; nothing is launched)."""
+    torch = pytest.importorskip("torch")
+    q = torch.zeros(1, 2, 4 * 8, 64, dtype=torch.bfloat16)
+    small = torch.zeros(1, 2, 4 * 8 - 8, 64, dtype=torch.bfloat16)
+    mask = np.ones((4, 4), np.uint8)
+    for args in ((q, small, q), (q, q, small)):
+        with pytest.raises(ValueError, match="shape"):
+            ta.tile_attn(*args, mask, T=8)
+        with pytest.raises(ValueError, match="shape"):
+            ta.dense_attn(*args, T=8)
+    with pytest.raises(ValueError, match="shape"):
+        ta.tile_attn(q, q, q, mask, T=8, out=small)
+    with pytest.raises(ValueError, match="GPU"):
+        ta.tile_attn(q, q, q, mask, T=8)
+
+
+def test_bf16_rounding_of_the_input_recipe():
+    """workloads.f32_to_bf16_bits rounds to nearest, ties to even (torch's float32 ->
+    bfloat16 conversion), across the pieces it works through."""
+    torch = pytest.importorskip("torch")
+    import workloads
+
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((1 << 20) + 77).astype(np.float32) * 10.0 ** rng.integers(-6, 6, (1 << 20) + 77)
+    x = x.astype(np.float32)
+    ties = (np.arange(1, 2001, dtype=np.uint32) << 16 | 0x8000).view(np.float32)  # exact halfway values
+    x = np.concatenate([x, ties, -ties, np.float32([0.0, -0.0, 1.0, 3.4e38])])
+    got = workloads.f32_to_bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, ref)
+    with pytest.raises(ValueError):
+        workloads.f32_to_bf16_bits(np.float32([1.0, np.nan]))
+

@@ -9,10 +9,11 @@ import numpy as np
 import pytest
 
 import workloads
+from oracle import attention as oa
 from oracle import backward as ob
 from oracle import masks as om
 from oracle import mmdit as ommd
-from tests.gpu_helpers import from_dev, to_dev, widen
+from tests.gpu_helpers import from_dev, to_dev, upstream_grad, widen, workload_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -38,6 +39,7 @@ def grad_errors(got_bits, ref):
     rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
     return {
         "max_abs": float(diff.max()) if diff.size else 0.0,
+        "mean_abs": float(diff.mean()) if diff.size else 0.0,
         "max_rel": float(diff.max()) / peak if peak > 0 else float(diff.max() if diff.size else 0.0),
         "rel_rms": float(np.sqrt(np.mean(diff * diff))) / rms if rms > 0 else 0.0,
         "peak": peak,
@@ -216,31 +218,49 @@ def test_bwd_last_key_block_full_frames():
     full_check(qb, kb, vb, gb, om.tile_mask(F, 1, "col"), T, d ** -0.5, "bwd-3600")
 
 
-# Every workload the benchmark times for the gradients: the 93-frame and 29-frame shapes,
-# the frame-correlated sweep data, one GPU's head share, the 48-frame long horizon (T =
-# 1200, two global frames) and 128-wide heads (split dV and dK key-side passes).
-FULL_CASES = [("93f", "col", 1), ("93f", "sym", 1), ("29f", "col", 1), ("sweep", "sym", 2),
-              ("sp_share", "sym", 1), ("long", "col", 2), ("93f_d128", "col", 1)]
+# Every (workload, mask form, g) the benchmark times for the gradients (bench.py
+# ALL_CASES with --pass bwd), with the dense control of each workload: the 93-frame and
+# 29-frame shapes, the frame-correlated sweep data, one GPU's head share, the 48-frame
+# long horizon (T = 1200, two global frames) and 128-wide heads (split dV and dK
+# key-side passes). Rows of the masks with many kept pairs per key check dk and dv on
+# one head, to keep the float64 oracle's work per case near the others'.
+FULL_CASES = [
+    ("29f", "col", 1), ("29f", "sym", 1), ("29f", "dense", 0),
+    ("93f", "col", 1), ("93f", "sym", 1), ("93f", "dense", 0),
+    ("sweep", "col", 1), ("sweep", "col", 2), ("sweep", "col", 4), ("sweep", "col", 8),
+    ("sweep", "sym", 2), ("sweep", "sym", 4), ("sweep", "sym", 8), ("sweep", "dense", 0),
+    ("sp_share", "col", 1), ("sp_share", "sym", 1), ("sp_share", "dense", 0),
+    ("long", "col", 2), ("long", "sym", 2), ("long", "dense", 0),
+    ("93f_d128", "col", 1), ("93f_d128", "sym", 1), ("93f_d128", "dense", 0),
+]
 
 
-@pytest.mark.parametrize("name,form,g", FULL_CASES, ids=[f"{a}-{b}-g{c}" for a, b, c in FULL_CASES])
+def _bwd_full(name, form, g):
+    w = workloads.WORKLOADS[name]
+    qb, kb, vb = workload_inputs(name)
+    gb = upstream_grad(qb.shape, 98)
+    mask = np.ones((w.F, w.F), np.uint8) if form == "dense" else om.tile_mask(w.F, g, form)
+    return w, qb, kb, vb, gb, mask, run_gpu_bwd(qb, kb, vb, gb, mask, w.T, w.scale())
+
+
+@pytest.mark.parametrize("name,form,g", [c for c in FULL_CASES if c[1] != "dense" or c[0] == "29f"],
+                         ids=[f"{a}-{b}-g{c}" for a, b, c in FULL_CASES if b != "dense" or a == "29f"])
 def test_bwd_full_size_sampled(name, form, g):
     """The measured shapes in the benchmark's launch configuration: dq on sampled
     query rows and dk, dv on sampled key rows (the heavy global frame 0, an ordinary
-    frame and the last frame, including each frame's ragged last rows) of two heads."""
-    w = workloads.WORKLOADS[name]
+    frame and the last frame, including each frame's ragged last rows)."""
     print(f"[case] bwd full {name} {form} g={g}", flush=True)
-    qb, kb, vb = workloads.make_workload_qkv(w)
-    gb = make_grad(w.B, w.H, w.F * w.T, w.d, 98)
-    mask = om.tile_mask(w.F, g, form)
-    dq, dk, dv = run_gpu_bwd(qb, kb, vb, gb, mask, w.T, w.scale())
+    w, qb, kb, vb, gb, mask, (dq, dk, dv) = _bwd_full(name, form, g)
     rng = np.random.default_rng(99)
     heads = [0, w.H - 1]
+    # a key row's gradient sums over every query frame that keeps its frame
+    key_heads = heads if np.count_nonzero(mask) <= 2 * 70 else heads[:1]
     rows_q, rows_k = [], []
     for h in heads:
         for f in range(w.F):
             for r in {0, w.T - 1, int(rng.integers(0, w.T))}:
                 rows_q.append((0, h, f * w.T + r))
+    for h in key_heads:
         for f in (0, 1, w.F - 1):
             for r in {0, 255, 256, w.T - 17, w.T - 1, int(rng.integers(0, w.T))}:
                 rows_k.append((0, h, f * w.T + r))
@@ -252,6 +272,54 @@ def test_bwd_full_size_sampled(name, form, g):
     assert_grad(dv[bk, hk, sk], rv, f"{name}-{form}-dv")
     for x in (dq, dk, dv):
         assert np.all(np.isfinite(widen(x[:, :, :: max(1, w.T // 7)])))
+
+
+@pytest.mark.parametrize("name", [c[0] for c in FULL_CASES if c[1] == "dense" and c[0] != "29f"])
+def test_bwd_dense_full_size(name):
+    """The dense control's gradients at the full shapes (the 29-frame one is checked row
+    by row above). dq on sampled query rows of two heads against the oracle; a key row's
+    oracle gradient would need the whole attention of its head (about 3e12 float64
+    FLOP at 93 frames), so dk and dv are checked, over every head, by two identities
+    that hold for any mask at any size:
+      - the scores' gradients of one query sum to zero over its kept keys
+        (sum_t dS_st = D_s - D_s), so the keys' dk sum to zero;
+      - the attention weights of one query sum to one, so the keys' dv sum to the sum
+        of dO over the queries.
+    In bf16 the first sum moves off zero mainly through delta, which is formed from
+    the bf16 forward output: D_s errs by about 2^-8 |O_s| |dO_s| / sqrt(3), and these
+    errors enter sum_t dk_t weighted by scale * q_s with random signs. The bound takes
+    |O_s| from the oracle's rows, plus the bf16 rounding of the S summed rows. Dropping
+    delta altogether moves the sum by |D_s| itself, about 90 times further."""
+    print(f"[case] bwd dense full {name}", flush=True)
+    w, qb, kb, vb, gb, mask, (dq, dk, dv) = _bwd_full(name, "dense", 0)
+    rng = np.random.default_rng(100)
+    rows_q = [(0, h, f * w.T + r) for h in (0, w.H - 1) for f in range(w.F)
+              for r in {0, w.T - 1, int(rng.integers(0, w.T))}]
+    bq, hq, sq = (np.array(x) for x in zip(*rows_q))
+    empty = np.zeros(0, np.int64)
+    rq, _, _ = ob.attention_backward_rows(qb, kb, vb, gb, mask, w.T, w.scale(), bq, hq, sq,
+                                          empty, empty, empty)
+    assert_grad(dq[bq, hq, sq], rq, f"{name}-dense-dq")
+    o_rows = oa.attention_rows(qb, kb, vb, mask, w.T, w.scale(), bq, hq, sq)
+    o_norm = float(np.sqrt(np.mean(np.sum(o_rows ** 2, axis=1))))
+    worst_k = worst_v = 0.0
+    for b in range(w.B):
+        for h in range(w.H):
+            dk64, dv64, g64, q64 = (widen(x[b, h]) for x in (dk, dv, gb, qb))
+            do_norm = float(np.sqrt(np.mean(np.sum(g64 ** 2, axis=1))))
+            rms_dk = float(np.sqrt(np.mean(dk64 ** 2)))
+            rms_dv = float(np.sqrt(np.mean(dv64 ** 2)))
+            rounding = np.sqrt(w.S) * 2.0 ** -9
+            tol_k = 6 * (w.scale() * 2.0 ** -8 * o_norm * do_norm / np.sqrt(3)
+                         * np.sqrt(np.sum(q64 ** 2, axis=0)) + rounding * rms_dk)
+            tol_v = 8 * 2 * rounding * rms_dv + 1e-3
+            err_k = np.abs(dk64.sum(axis=0))
+            err_v = np.abs(dv64.sum(axis=0) - g64.sum(axis=0))
+            worst_k = max(worst_k, float(np.max(err_k / tol_k)))
+            worst_v = max(worst_v, float(np.max(err_v / tol_v)))
+    print(f"[grad] {name}-dense sums over keys: |sum dk| / bound {worst_k:.3f}, "
+          f"|sum dv - sum dO| / bound {worst_v:.3f} (|O| {o_norm:.3e})", flush=True)
+    assert worst_k <= 1.0 and worst_v <= 1.0
 
 
 # ---- the MM-DiT form (text prefix) ------------------------------------------------------
@@ -295,15 +363,16 @@ def test_bwd_mmdit_without_text_matches_plain_bitwise():
         assert np.array_equal(x, y)
 
 
-@pytest.mark.parametrize("k", [1, 12])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 6, 12, 0])
 def test_bwd_mmdit_cog_shape_sampled(k):
     """CogVideoX-5B shape (226 text tokens, 13 x 1350 video tokens, 48 heads of 64),
-    sym masks: text and video query rows and key rows (text keys are kept by every
+    sym masks with k global frames (every mask the benchmark times; k = 0 is the dense
+    control): text and video query rows and key rows (text keys are kept by every
     query) of two heads."""
     w = workloads.WORKLOADS["cog"]
-    qb, kb, vb = workloads.make_workload_qkv(w)
-    gb = make_grad(w.B, w.H, w.S, w.d, 103)
-    mask = om.tile_mask(w.F, k, "sym")
+    qb, kb, vb = workload_inputs("cog")
+    gb = upstream_grad(qb.shape, 103)
+    mask = om.tile_mask(w.F, k, "sym") if k else np.ones((w.F, w.F), np.uint8)
     print(f"[case] bwd cog k={k}", flush=True)
     dq, dk, dv = run_gpu_bwd_mmdit(qb, kb, vb, gb, mask, w.T, w.prefix, w.scale())
     rng = np.random.default_rng(k)

@@ -7,7 +7,7 @@ import workloads
 from oracle import attention as oa
 from oracle import masks as om
 from oracle import mmdit as ommd
-from tests.gpu_helpers import assert_parity, from_dev, to_dev
+from tests.gpu_helpers import assert_parity, from_dev, to_dev, workload_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -107,14 +107,15 @@ def test_mmdit_skipped_video_frames_are_never_read():
     assert_parity(base, ommd.attention_mmdit(qb, kb, vb, mask, T, P, 0.125), "mmdit-poison-base")
 
 
-@pytest.mark.parametrize("k", [1, 3, 12])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 6, 12, 0])
 def test_mmdit_cog_shape_sampled(k):
     """CogVideoX-5B shape (App. E reading: 13 latent frames x 1350 tokens, 226 text
-    tokens, 48 heads of 64), sym masks with k global frames (labels 12, 4, 1 of
-    tab:cog_kernel): every text row and sampled video rows of three heads."""
+    tokens, 48 heads of 64), sym masks with k global frames (labels 12, 6, 4, 3, 2, 1
+    of tab:cog_kernel; k = 0 stands for the dense control, every tile kept): every text
+    row and sampled video rows of three heads."""
     w = workloads.WORKLOADS["cog"]
-    qb, kb, vb = workloads.make_workload_qkv(w)
-    mask = om.tile_mask(w.F, k, "sym")
+    qb, kb, vb = workload_inputs("cog")
+    mask = om.tile_mask(w.F, k, "sym") if k else np.ones((w.F, w.F), np.uint8)
     print(f"[case] cog k={k}", flush=True)
     got, lse = run_mmdit(qb, kb, vb, mask, w.T, w.prefix, w.scale())
     rng = np.random.default_rng(k)

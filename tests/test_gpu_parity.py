@@ -11,7 +11,8 @@ import pytest
 import workloads
 from oracle import attention as oa
 from oracle import masks as om
-from tests.gpu_helpers import assert_parity, errors, from_dev, sample_rows, to_dev
+from tests.gpu_helpers import (assert_parity, errors, from_dev, sample_rows, to_dev,
+                               workload_inputs)
 
 pytestmark = pytest.mark.gpu
 
@@ -191,24 +192,16 @@ def test_many_frames_short_tiles():
 
 # ---- measured workloads at full size, sampled rows --------------------------------
 
-_CACHE = {}
-
-
-def _inputs(w):
-    key = (w.B, w.H, w.F, w.T, w.d, w.seed, w.dist)
-    if key not in _CACHE:
-        _CACHE.clear()
-        _CACHE[key] = workloads.make_workload_qkv(w)
-    return _CACHE[key]
-
-
+# Every (workload, mask form, g) the benchmark times (bench.py ALL_CASES), with the
+# dense control of each workload.
 FULL_CASES = [
     ("29f", "col", 1), ("29f", "sym", 1), ("29f", "dense", 1),
     ("93f", "col", 1), ("93f", "sym", 1), ("93f", "dense", 1),
-    ("sweep", "col", 2), ("sweep", "sym", 2), ("sweep", "col", 4), ("sweep", "sym", 8),
-    ("sweep", "dense", 1),
-    ("sp_share", "col", 1), ("long", "col", 2), ("long", "sym", 2),
-    ("93f_d128", "col", 1), ("93f_d128", "sym", 1),
+    ("sweep", "col", 1), ("sweep", "col", 2), ("sweep", "col", 4), ("sweep", "col", 8),
+    ("sweep", "sym", 2), ("sweep", "sym", 4), ("sweep", "sym", 8), ("sweep", "dense", 1),
+    ("sp_share", "col", 1), ("sp_share", "sym", 1), ("sp_share", "dense", 1),
+    ("long", "col", 2), ("long", "sym", 2), ("long", "dense", 2),
+    ("93f_d128", "col", 1), ("93f_d128", "sym", 1), ("93f_d128", "dense", 1),
 ]
 
 
@@ -216,7 +209,7 @@ FULL_CASES = [
 def test_full_size_sampled(name, form, g):
     w = workloads.WORKLOADS[name]
     print(f"[case] full {name} {form} g={g}", flush=True)
-    qb, kb, vb = _inputs(w)
+    qb, kb, vb = workload_inputs(name)
     mask = om.tile_mask(w.F, g, form)
     got = run_gpu(qb, kb, vb, mask, w.T, w.scale())
     heads = None if form != "dense" else [0, w.H // 2, w.H - 1]
@@ -394,7 +387,7 @@ def test_per_head_masks_full_size_sampled():
     """93-frame 720p shape with a different k:(F-k) pattern per head (col and sym, g = 1,
     2, 4, 8): sampled rows of every head, and the log-sum-exp of two heads in full."""
     w = workloads.WORKLOADS["93f"]
-    qb, kb, vb = _inputs(w)
+    qb, kb, vb = workload_inputs("93f")
     masks = np.stack([om.tile_mask(w.F, [1, 2, 4, 8][h % 4], "col" if h % 2 else "sym")
                       for h in range(w.H)])
     got, lse = run_gpu_heads(qb, kb, vb, masks, w.T, w.scale())

@@ -68,14 +68,24 @@ WORKLOADS = {
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round finite float32 values to bf16 (round to nearest, ties to even).
 
-    Returns the bf16 bit patterns as uint16.
+    Returns the bf16 bit patterns as uint16. Works through the array in pieces of
+    2^20 values, which keeps the temporaries in cache for the large workloads.
     """
     x = np.ascontiguousarray(x, dtype=np.float32)
-    if not np.all(np.isfinite(x)):
-        raise ValueError("only finite values are converted")
-    u = x.view(np.uint32)
-    bias = ((u >> 16) & 1) + np.uint32(0x7FFF)
-    return ((u + bias) >> 16).astype(np.uint16)
+    flat = x.reshape(-1)
+    u = flat.view(np.uint32)
+    out = np.empty(u.shape, dtype=np.uint16)
+    step = 1 << 20
+    for i in range(0, u.size, step):
+        if not np.all(np.isfinite(flat[i:i + step])):
+            raise ValueError("only finite values are converted")
+        c = u[i:i + step]
+        r = (c >> np.uint32(16)) & np.uint32(1)
+        r += np.uint32(0x7FFF)
+        r += c
+        r >>= np.uint32(16)
+        out[i:i + step] = r
+    return out.reshape(x.shape)
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
