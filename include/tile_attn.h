@@ -64,6 +64,8 @@ extern "C" {
 
 #define TA_MAX_FRAMES 1024
 #define TA_PLAN_CACHE_ENTRIES 256
+#define TA_NOALLOC_PLAN_WORDS 65536
+#define TA_NOALLOC_PARTIAL_BYTES (64u << 20)
 
 typedef enum {
   TA_OK = 0,
@@ -243,6 +245,31 @@ int tile_attn_compact(const uint8_t* tile_mask, int F, int32_t* row_ptr,
  */
 int tile_attn_plan(const uint8_t* tile_mask, int F, int32_t* items, int cap, int* n_items,
                    int* n_slots);
+
+/*
+ * tile_attn_fwd_heads for callers that cannot allocate device memory: code being
+ * captured into a HIP graph, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, results and errors as tile_attn_fwd_heads, but the call allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine): its work plan and
+ * the partial results of split query frames live in one static device array per GPU,
+ * TA_NOALLOC_PLAN_WORDS int32 words for the plan plus TA_NOALLOC_PARTIAL_BYTES for
+ * the partials (about 64.25 MiB), held from the library's first use on a GPU until
+ * the process ends. The plan reaches the array by value, in the arguments of small
+ * store kernels enqueued on `stream`, so the call only enqueues kernels and reads no
+ * host memory after it returns.
+ *
+ * Every call on one GPU shares that GPU's array, so calls whose execution overlaps
+ * on one GPU (on different streams, or graphs replayed concurrently) race: order
+ * them on one stream. A mask whose split plan needs more partial space than the
+ * array holds runs unsplit (each heavy query frame as one work item; same results up
+ * to rounding order, the heavy rows then set the launch's critical path).
+ * Errors: those of tile_attn_fwd_heads; TA_ERR_BAD_SHAPE also when the plan exceeds
+ * TA_NOALLOC_PLAN_WORDS words (about 5 * H * F + nnz of all masks).
+ */
+int tile_attn_fwd_heads_noalloc(const void* q, const void* k, const void* v, void* out,
+                                int B, int H, int F, int T, int d,
+                                const uint8_t* tile_masks, int n_masks, float scale,
+                                float* lse, void* stream);
 
 /*
  * Occupancy of the plan cache (all devices): *live receives the number of cached

@@ -17,6 +17,7 @@ from .api import (  # noqa: F401
     tile_attn_compact,
     tile_attn_fwd,
     tile_attn_fwd_heads,
+    tile_attn_fwd_heads_noalloc,
     tile_attn_fwd_mmdit,
     tile_attn_make_mask,
     tile_attn_plan,

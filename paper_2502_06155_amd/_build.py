@@ -10,7 +10,8 @@ REPO_DIR = os.path.dirname(PKG_DIR)
 CSRC = os.path.join(PKG_DIR, "csrc")
 LIB_NAME = "libtileattn.so"
 LIB_PATH = os.path.join(PKG_DIR, LIB_NAME)
-SOURCES = [os.path.join(CSRC, f) for f in ("tile_attn_host.cpp", "tile_attn_kernels.hip", "tile_attn_bwd.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("tile_attn_host.cpp", "tile_attn_kernels.hip", "tile_attn_bwd.hip",
+                                               "tile_attn_noalloc.hip")]
 
 HIP_FLAGS = [
     "--offload-arch=gfx950",

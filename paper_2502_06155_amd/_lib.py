@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtileattn
 EXPORTS = (
     "tile_attn_fwd",
     "tile_attn_fwd_heads",
+    "tile_attn_fwd_heads_noalloc",
     "tile_attn_fwd_mmdit",
     "tile_attn_bwd",
     "tile_attn_bwd_mmdit",
@@ -54,6 +55,8 @@ def _load() -> ctypes.CDLL:
     lib.tile_attn_fwd.restype = ci
     lib.tile_attn_fwd_heads.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, vp, ci, cf, vp, vp]
     lib.tile_attn_fwd_heads.restype = ci
+    lib.tile_attn_fwd_heads_noalloc.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, vp, ci, cf, vp, vp]
+    lib.tile_attn_fwd_heads_noalloc.restype = ci
     lib.tile_attn_fwd_mmdit.argtypes = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, vp, ci, cf, vp, vp]
     lib.tile_attn_fwd_mmdit.restype = ci
     lib.tile_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, ci, ci, ci, ci, ci, vp, ci,

@@ -74,6 +74,19 @@ def tile_attn_fwd_heads(q, k, v, out, B: int, H: int, F: int, T: int, d: int, ti
                                    _stream(stream)), "tile_attn_fwd_heads")
 
 
+def tile_attn_fwd_heads_noalloc(q, k, v, out, B: int, H: int, F: int, T: int, d: int, tile_masks,
+                                scale: float, lse=None, stream=None) -> None:
+    """tile_attn_fwd_heads_noalloc of the C ABI: tile_attn_fwd_heads without any device
+    allocation (plan and partials in the library's static per-GPU scratch array)."""
+    m = np.ascontiguousarray(np.asarray(tile_masks), dtype=np.uint8)
+    if m.size % (F * F):
+        raise ValueError("tile_masks must hold n_masks * F * F entries")
+    n_masks = m.size // (F * F)
+    _check(lib.tile_attn_fwd_heads_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, F, T, d,
+                                           m.ctypes.data, n_masks, float(scale), _ptr(lse),
+                                           _stream(stream)), "tile_attn_fwd_heads_noalloc")
+
+
 def tile_attn_fwd_mmdit(q, k, v, out, B: int, H: int, F: int, T: int, P: int, d: int,
                         tile_masks, scale: float, lse=None, stream=None) -> None:
     """tile_attn_fwd_mmdit of the C ABI: P text tokens before the F*T video tokens

@@ -276,3 +276,16 @@ def test_bf16_rounding_of_the_input_recipe():
     with pytest.raises(ValueError):
         workloads.f32_to_bf16_bits(np.float32([1.0, np.nan]))
 
+
+def test_noalloc_rejects_a_plan_beyond_its_scratch_before_any_gpu_call():
+    """tile_attn_fwd_heads_noalloc refuses a plan of more than TA_NOALLOC_PLAN_WORDS words
+    before anything is enqueued (the buffers are fake addresses that nothing touches)."""
+    B, H, F, T, d = 1, 128, 128, 64, 64
+    masks = np.ones((H, F, F), np.uint8)  # 5 * 128 * 128 item words + 128^3 kept entries
+    fake = 1 << 40
+    with pytest.raises(ta.TileAttnError, match="static scratch"):
+        ta.tile_attn_fwd_heads_noalloc(fake, fake + (1 << 30), fake + (2 << 30), fake + (3 << 30),
+                                       B, H, F, T, d, masks, 0.125, None, None)
+    with open(os.path.join(ROOT, "include", "tile_attn.h")) as f:
+        hdr = f.read()
+    assert "#define TA_NOALLOC_PLAN_WORDS 65536" in hdr
