@@ -149,8 +149,10 @@ def cpu_baseline(w, qb, kb, vb, mask, budget_s: float):
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"float64 oracle on heads 0..{done - 1} of {w.H} (all {w.F} query frames, "
-                  f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles; {cpu_model()}",
+        "sample": f"float64 numpy oracle (the parity reference, kept in float64 so its rounding "
+                  f"is negligible next to bf16) on heads 0..{done - 1} of {w.H} (all {w.F} query "
+                  f"frames, b=0) of the same problem, {dt:.1f} s; throughput over kept tiles; "
+                  f"{cpu_model()}",
     }
 
 
@@ -184,8 +186,9 @@ def cpu_baseline_bwd(w, qb, kb, vb, gb, mask, budget_s: float):
         "unit": "TFLOP/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"float64 gradient oracle on heads 0..{done - 1} of {w.H} (all {w.F} frames, "
-                  f"b=0) of the same problem, {dt:.1f} s; throughput over kept tiles; {cpu_model()}",
+        "sample": f"float64 numpy gradient oracle (the parity reference) on heads 0..{done - 1} of "
+                  f"{w.H} (all {w.F} frames, b=0) of the same problem, {dt:.1f} s; throughput over "
+                  f"kept tiles; {cpu_model()}",
     }
 
 
