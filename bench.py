@@ -38,10 +38,12 @@ KERNEL_SRCS = {
     "fwd": [os.path.join(CSRC, f) for f in ("tile_attn_kernels.hip", "tile_common.h", "launch.h")],
     "bwd": [os.path.join(CSRC, f) for f in ("tile_attn_bwd.hip", "tile_common.h", "launch.h")],
 }
-PROFILE_MD = {
-    "fwd": os.path.join(ROOT, "profiles", "tile_attn_fwd_93f_col_g1.md"),
-    "bwd": os.path.join(ROOT, "profiles", "tile_attn_bwd_93f_col_g1.md"),
-}
+
+
+def profile_md(which: str = "fwd", workload: str = "93f", form: str = "col", g: int = 1) -> str:
+    """The committed rocprofv3 summary of one pass of one workload and mask:
+    profiles/tile_attn_<pass>_<workload>_<form>_g<g>.md."""
+    return os.path.join(ROOT, "profiles", f"tile_attn_{which}_{workload}_{form}_g{g}.md")
 
 
 def log(*a):
@@ -84,15 +86,18 @@ def paper_stat(per_call):
     return float(np.median(a)), float(band.mean() if band.size else a.mean())
 
 
-def profile_record(which: str = "fwd", key: str = "hbm_bytes_per_launch"):
-    """One per-launch figure of the committed rocprofv3 counter summary, or None when
-    the summary was taken on other kernel sources. hbm_bytes_per_launch: HBM bytes
-    (FETCH_SIZE and WRITE_SIZE, each calibrated on a plain copy of known size);
-    mfma_bf16_flop_per_launch: SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP per op."""
-    if not os.path.exists(PROFILE_MD[which]):
+def profile_record(which: str = "fwd", key: str = "hbm_bytes_per_launch", workload: str = "93f",
+                   form: str = "col", g: int = 1):
+    """One per-launch figure of the committed rocprofv3 counter summary of this pass,
+    workload and mask, or None when there is none or it was taken on other kernel
+    sources. hbm_bytes_per_launch: HBM bytes (FETCH_SIZE and WRITE_SIZE, each
+    calibrated on a plain copy of known size); mfma_bf16_flop_per_launch:
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP per op."""
+    path = profile_md(which, workload, form, g)
+    if not os.path.exists(path):
         return None
     rec = {}
-    with open(PROFILE_MD[which]) as f:
+    with open(path) as f:
         for line in f:
             if ":" in line and not line.startswith(("|", "#", " ", "`")):
                 k, _, val = line.partition(":")
@@ -103,9 +108,9 @@ def profile_record(which: str = "fwd", key: str = "hbm_bytes_per_launch"):
     return float(rec[key])
 
 
-def traffic_from_profile(which: str = "fwd"):
+def traffic_from_profile(which: str = "fwd", workload: str = "93f", form: str = "col", g: int = 1):
     """HBM bytes per launch of the dominant kernel(s), or None (see profile_record)."""
-    return profile_record(which, "hbm_bytes_per_launch")
+    return profile_record(which, "hbm_bytes_per_launch", workload, form, g)
 
 
 def cpu_model() -> str:
@@ -455,19 +460,19 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
-            "traffic": traffic_from_profile(which),
+            "traffic": traffic_from_profile(which, w.name, args.form, g),
         },
         "cpu_baseline": cpu,
         "gemm_reference": gemm,
     }
     # Matrix work the counters saw (padding included) over the same measured time.
-    mfma_flop = profile_record(which, "mfma_bf16_flop_per_launch")
+    mfma_flop = profile_record(which, "mfma_bf16_flop_per_launch", w.name, args.form, g)
     if mfma_flop is not None:
         ctf = mfma_flop / (np.mean(per) * 1e-3) / 1e12
         line["mfma_counter"] = {"flop_per_launch": mfma_flop, "tflops": ctf,
                                 "frac": ctf / PEAK_BF16_TFLOPS,
                                 "source": "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, "
-                                          + os.path.relpath(PROFILE_MD[which], ROOT)}
+                                          + os.path.relpath(profile_md(which, w.name, args.form, g), ROOT)}
     line.update(extra)
     print(json.dumps(line), flush=True)
 

@@ -7,8 +7,8 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-PROFILES = ["tile_attn_fwd_93f_col_g1.md", "tile_attn_bwd_93f_col_g1.md",
-            "tile_attn_fwd_mmdit_cog_sym_g1.md"]
+PROFILES = sorted(f for f in os.listdir(os.path.join(ROOT, "profiles"))
+                  if f.startswith("tile_attn_") and f.endswith(".md"))
 
 
 @pytest.mark.parametrize("name", PROFILES)
@@ -36,3 +36,17 @@ def test_bench_parser_reads_the_fwd_record():
     # the record is returned when the hash matches the sources, None otherwise
     got = bench.profile_record("fwd", "mfma_bf16_flop_per_launch")
     assert got is None or got > 5.0e12
+    got = bench.profile_record("fwd", "mfma_bf16_flop_per_launch", "29f", "col", 1)
+    assert got is None or got > 1.7e12
+
+
+def test_every_summary_is_named_for_its_pass_workload_and_mask():
+    import bench
+    import workloads
+
+    assert len(PROFILES) >= 5
+    for name in PROFILES:
+        m = re.fullmatch(r"tile_attn_(fwd|bwd)_(\w+)_(col|sym|dense)_g(\d+)\.md", name)
+        assert m, name
+        assert m.group(2) in workloads.WORKLOADS, name
+        assert bench.profile_md(m.group(1), m.group(2), m.group(3), int(m.group(4))).endswith(name)
