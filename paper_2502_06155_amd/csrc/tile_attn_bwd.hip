@@ -580,21 +580,36 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
       constexpr int buf = decltype(bufc)::value;
       if (t + 1 < n_tiles) load_tile(nxt, buf ^ 1);
       if (wave_active) {
-        if constexpr (MODE == kDkDv) {
-          // One stream of 8 D/16 MFMAs, each in a fenced packet with its share of the
-          // vector work; the operand fragment of MFMA i is read from LDS at packet
-          // i - 2 into one of three rotating registers, so no MFMA waits on a read
-          // issued just before it (3.5% faster than leaving the order to the
-          // compiler). Stream: S and dP of half 0, S and dP of half 1 (with half 0's
-          // P and dS forming), the dV/dK update of half 0 (with half 1's P and dS
-          // forming), the update of half 1.
+        if constexpr (MODE != kDkOnly) {
+          // One stream of MFMAs (8 D/16 per tile for dV and dK together), each in a
+          // fenced packet with its share of the vector work; the operand fragment of
+          // MFMA i is read from LDS at packet i - 2 into one of three rotating
+          // registers, so no MFMA waits on a read issued just before it (3.5% faster
+          // than leaving the order to the compiler). Stream: S (and dP) of half 0, S
+          // (and dP) of half 1 with half 0's P (and dS) forming, the dV/dK update of
+          // half 0 with half 1's P (and dS) forming, the update of half 1. The dV pass
+          // of d = 128 (S, P, dV) runs the same stream without dP, dS and dK; the dK
+          // pass (S, dP, dS, dK) would need three registers more than it has.
           constexpr int kC = Sh::kChunks, kMb = Sh::kDBlocks;
-          constexpr int kHalf = 2 * kC;             // S + dP MFMAs of a half
-          constexpr int kAcc = 4 * kMb;             // dV + dK MFMAs of a half
-          constexpr int kN = 2 * kHalf + 2 * kAcc;  // the whole stream
-          f32x16 sc[2], dp[2];
-          bf16x8 pb[2][2], db[2][2];
+          constexpr int kHalf = (kWantDk ? 2 : 1) * kC;                   // S (+ dP) MFMAs of a half
+          constexpr int kAcc = ((int)kWantDv + (int)kWantDk) * 2 * kMb;  // update MFMAs of a half
+          constexpr int kN = 2 * kHalf + 2 * kAcc;                        // the whole stream
+          constexpr int kPerC2 = kAcc / 2;                                 // update MFMAs per chunk
+          f32x16 sc[2], dp[kWantDk ? 2 : 1];
+          bf16x8 pb[kWantDv ? 2 : 1][2], db[kWantDk ? 2 : 1][2];
           f32x4 l4[2][4];  // lse2 of this lane's 16 queries of each half, 4 at a time
+          // Update MFMA r of a half: chunk c2, d-block mb, dK (else dV).
+          auto upd = [](int r, int& c2, int& mb, bool& is_dk) {
+            c2 = r / kPerC2;
+            const int q = r % kPerC2;
+            if (kWantDv && kWantDk) {
+              mb = q / 2;
+              is_dk = q % 2;
+            } else {
+              mb = q;
+              is_dk = kWantDk;
+            }
+          };
           auto frag = [&](auto ic) -> bf16x8 {
             constexpr int i = decltype(ic)::value;
             if constexpr (i < 2 * kHalf) {
@@ -603,7 +618,9 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
               else return row_frag<D>(sG[buf], ra, h, r - kC);
             } else {
               constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
-              constexpr int c2 = r / (2 * kMb), mb = (r % (2 * kMb)) / 2, is_dk = r % 2;
+              int c2, mb;
+              bool is_dk;
+              upd(r, c2, mb, is_dk);
               return tr_frag<D>(is_dk ? sQ[buf] : sG[buf], ta, mb, 2 * h + c2);
             }
           };
@@ -612,20 +629,28 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
             if constexpr (i < 2 * kHalf) {
               constexpr int h = i / kHalf, r = i % kHalf;
               if constexpr (r < kC) sc[h] = mfma32(f, kf[r], r == 0 ? f32x16{} : sc[h]);
-              else dp[h] = mfma32(f, vf[r - kC], dp[h]);
+              else if constexpr (kWantDk) dp[h] = mfma32(f, vf[r - kC], dp[h]);
             } else {
               constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
-              constexpr int c2 = r / (2 * kMb), mb = (r % (2 * kMb)) / 2, is_dk = r % 2;
-              if constexpr (is_dk) dk[mb] = mfma32(f, db[h][c2], dk[mb]);
-              else dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
+              int c2, mb;
+              bool is_dk;
+              upd(r, c2, mb, is_dk);
+              if constexpr (kWantDk && kWantDv) {
+                if (is_dk) dk[mb] = mfma32(f, db[h][c2], dk[mb]);
+                else dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
+              } else if constexpr (kWantDk) {
+                dk[mb] = mfma32(f, db[h][c2], dk[mb]);
+              } else {
+                dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
+              }
             }
           };
           // Vector work of packet i: LDS reads of -delta (dP starts) and lse2 ahead of
-          // their use, and P, dS of half 0 over the second half's S/dP packets, of half
-          // 1 over half 0's update packets, 2 queries at a time.
+          // their use, and P (and dS) of half 0 over the second half's S/dP packets, of
+          // half 1 over half 0's update packets, 2 queries at a time.
           auto side = [&](auto ic) {
             constexpr int i = decltype(ic)::value;
-            if constexpr (i == 0 || i == kHalf) dp_start(buf, i / kHalf, dp[i / kHalf]);
+            if constexpr (kWantDk && (i == 0 || i == kHalf)) dp_start(buf, i / kHalf, dp[i / kHalf]);
             // lse2 of queries 4 q4 .. 4 q4 + 3 (entries 4 q4 ..) of half hh, read two
             // packets before the first packet whose share needs them.
             static_for<8>([&](auto qc) {
@@ -645,14 +670,20 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
                 const int e = 2 * u, c2 = e / 8, uu = (e % 8) / 4, j = e % 4;
                 const float p0 = prob(sc[h][e], a.c, l4[h][2 * c2 + uu][j]);
                 const float p1 = prob(sc[h][e + 1], a.c, l4[h][2 * c2 + uu][j + 1]);
-                const f32x2 pp = {p0, p1}, dd = {p0 * dp[h][e], p1 * dp[h][e + 1]};
-                const bf16x2 pq = __builtin_convertvector(pp, bf16x2);
-                const bf16x2 dq = __builtin_convertvector(dd, bf16x2);
-                u32x4 pw = __builtin_bit_cast(u32x4, pb[h][c2]), dw = __builtin_bit_cast(u32x4, db[h][c2]);
-                pw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, pq);
-                dw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, dq);
-                pb[h][c2] = __builtin_bit_cast(bf16x8, pw);
-                db[h][c2] = __builtin_bit_cast(bf16x8, dw);
+                if constexpr (kWantDv) {
+                  const f32x2 pp = {p0, p1};
+                  const bf16x2 pq = __builtin_convertvector(pp, bf16x2);
+                  u32x4 pw = __builtin_bit_cast(u32x4, pb[h][c2]);
+                  pw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, pq);
+                  pb[h][c2] = __builtin_bit_cast(bf16x8, pw);
+                }
+                if constexpr (kWantDk) {
+                  const f32x2 dd = {p0 * dp[h][e], p1 * dp[h][e + 1]};
+                  const bf16x2 dq = __builtin_convertvector(dd, bf16x2);
+                  u32x4 dw = __builtin_bit_cast(u32x4, db[h][c2]);
+                  dw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, dq);
+                  db[h][c2] = __builtin_bit_cast(bf16x8, dw);
+                }
               }
             }
           };
@@ -668,22 +699,18 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
             __builtin_amdgcn_sched_barrier(0);
           });
         } else {
-          // One of the two passes at d = 128: both halves' -delta reads, S, then dP
-          // (so the reads land while S forms), then half 0's P and dS and update
-          // ahead of half 1's; the compiler interleaves them (fencing the phases, as
-          // in the dq pass, measured 4% slower here).
+          // The dK pass at d = 128: both halves' -delta reads, S, then dP (so the reads
+          // land while S forms), then half 0's P and dS and update ahead of half 1's;
+          // the compiler interleaves them (fencing the phases, as in the dq pass,
+          // measured 4% slower here).
           f32x16 s0, dp0, s1, dp1;
           bf16x8 pb0[2], db0[2], pb1[2], db1[2];
-          if constexpr (kWantDk) {
-            dp_start(buf, 0, dp0);
-            dp_start(buf, 1, dp1);
-          }
+          dp_start(buf, 0, dp0);
+          dp_start(buf, 1, dp1);
           s_chain(buf, 0, s0);
           s_chain(buf, 1, s1);
-          if constexpr (kWantDk) {
-            dp_chain(buf, 0, dp0);
-            dp_chain(buf, 1, dp1);
-          }
+          dp_chain(buf, 0, dp0);
+          dp_chain(buf, 1, dp1);
           grads(buf, 0, s0, dp0, pb0, db0);
           accumulate(buf, 0, pb0, db0);
           grads(buf, 1, s1, dp1, pb1, db1);
