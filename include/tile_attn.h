@@ -31,15 +31,22 @@
  *   - Thread-safe. The first call for a given mask (per device) uploads its
  *     work plan (tile_attn_plan) with a blocking allocation and copy. Device
  *     copies of plans are cached, at most TA_PLAN_CACHE_ENTRIES of them (each
- *     4 * (5 * items + kept entries + 4 * split frames) bytes; a gradient call
- *     holds two: the mask's and its transpose's). Beyond that the least recently
+ *     4 * (5 * items + kept entries + 4 * split frames) bytes, plus for a forward
+ *     launch's schedule 128 bytes, 16 per part and 12 per query block cut into
+ *     parts; a gradient call holds two: the mask's and its transpose's; a forward
+ *     plan is cached per launch shape). Beyond that the least recently
  *     used one is evicted; its memory is freed only once no call holds it and
  *     events recorded after every call that used it have completed, so evicting
  *     never waits for a stream. A plan used while its stream is being captured
  *     into a graph is never evicted (the graph may replay at any later time). A
  *     mask whose plan splits heavy query frames also needs a workspace for the
  *     partial results, n_slots * B * max(T, P) * (d + 1) * 4 bytes (n_slots
- *     counts the pieces of all heads), held per (device, stream). A call that
+ *     counts the pieces of all heads), and so does a forward launch whose last
+ *     round of workgroups on some XCD would be ragged: where the plan splits no
+ *     frame, that round's query blocks are cut into parts over their kept tiles,
+ *     n_parts * R * (d + 4) * 4 bytes (R = 256 query rows per block, 128 at
+ *     d = 128; n_parts is at most 16 per block cut, and zero when the launch
+ *     fills whole rounds). The workspace is held per (device, stream). A call that
  *     needs more allocates a larger one (at least 1.5 times the size) and keeps
  *     the old one allocated until process exit, so no enqueued work ever sees
  *     its workspace freed and growing never waits for the stream. Later calls
@@ -249,7 +256,7 @@ int tile_attn_plan(const uint8_t* tile_mask, int F, int32_t* items, int cap, int
 /*
  * tile_attn_fwd_heads for callers that cannot allocate device memory: code being
  * captured into a HIP graph, tight serving loops, harnesses that forbid hipMalloc.
- * Same arguments, results and errors as tile_attn_fwd_heads, but the call allocates
+ * Same arguments and errors as tile_attn_fwd_heads, but the call allocates
  * nothing (no hipMalloc, hipFree or allocating library routine): its work plan and
  * the partial results of split query frames live in one static device array per GPU,
  * TA_NOALLOC_PLAN_WORDS int32 words for the plan plus TA_NOALLOC_PARTIAL_BYTES for
@@ -257,6 +264,9 @@ int tile_attn_plan(const uint8_t* tile_mask, int F, int32_t* items, int cap, int
  * the process ends. The plan reaches the array by value, in the arguments of small
  * store kernels enqueued on `stream`, so the call only enqueues kernels and reads no
  * host memory after it returns.
+ *
+ * It never cuts a launch's last round into parts, so where tile_attn_fwd_heads does,
+ * the two agree up to rounding order only (bit for bit otherwise).
  *
  * Every call on one GPU shares that GPU's array, so calls whose execution overlaps
  * on one GPU (on different streams, or graphs replayed concurrently) race: order

@@ -25,20 +25,39 @@ bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb);
 // words, read by the kernels with scalar loads. Items are {head, frame, first kept
 // entry, count, slot} with cols and slots offset per head; heavy entries are
 // {head, frame, first slot, slots}.
+// A forward plan also carries its launch schedule (FwdArgs::sched_*).
 struct DeviceWorkList {
   void* buffer = nullptr;
   const int32_t* items = nullptr;
   const int32_t* cols = nullptr;
   const int32_t* heavy = nullptr;
   int n_items = 0, n_heavy = 0, n_slots = 0;
+  const int32_t* sched_xcd = nullptr;
+  const int32_t* cut_units = nullptr;
+  int n_cut_units = 0, n_part_slots = 0, wg_per_xcd = 0;
 };
 
-// The same plan as host words, before upload: offsets of cols and heavy in words.
+// The same plan as host words, before upload: offsets of the parts in words.
 struct HostWorkList {
   std::vector<int32_t> words;
   size_t off_cols = 0, off_heavy = 0;
   int n_items = 0, n_heavy = 0, n_slots = 0;
+  size_t off_xcd = 0, off_pieces = 0, off_cut_units = 0;
+  int n_cut_units = 0, n_part_slots = 0, wg_per_xcd = 0;
 };
+
+// Workgroups a forward launch keeps resident per XCD (two per compute unit).
+int resident_slots_per_xcd(int dev);
+
+// Appends the forward launch schedule to hw (see FwdArgs::sched): B batch entries, nqb
+// query blocks of `rows` rows per segment, head dimension d, T tokens per frame and P
+// text tokens.
+// With share_tail, each XCD whose run would end in a ragged round of whole units (of
+// slots_x resident workgroups) runs that round's units in parts over the kept tiles
+// instead, one workgroup per part, merged by log-sum-exp; otherwise every unit is one
+// workgroup.
+void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int T, int P, int F,
+                         int slots_x, bool share_tail);
 
 // Plans H heads with n_masks masks (1: shared, H: one per head) of F segments; heavy
 // query frames are split into pieces when allow_split.

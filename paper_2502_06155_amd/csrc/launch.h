@@ -34,7 +34,15 @@ struct FwdArgs {
   float c;              // > 0: |scale| * log2(e), logits in base-2 units
   uint32_t qflip;       // 0x80008000 flips the sign of q (negative scale), else 0
   uint32_t qmask;       // 0 zeroes q (scale 0: exactly uniform weights), else ~0
-  uint32_t n_wg;        // B * n_items * ceil(max(T, P) / fwd_rows_per_workgroup(d))
+  // The launch schedule (on the device): per XCD (8 of them) {first unit, whole
+  // units, part workgroups, first piece}, then per part workgroup a piece {unit, first
+  // tile, tiles, partial slot}; and per unit run in parts {unit, first partial slot,
+  // parts}. Units are (b, item, query block), query block fastest.
+  const int32_t* sched;
+  const int32_t* cut_units;
+  int n_cut_units;
+  int wg_per_xcd;       // workgroups per XCD (the grid is 8 times that)
+  float* ws_parts;         // parts, fp32 [slot][fwd_rows_per_workgroup(d)][d + 4]: O/l, log-sum-exp
 };
 
 // Combines the partial results of split query frames: heavy holds 4 int32 per split

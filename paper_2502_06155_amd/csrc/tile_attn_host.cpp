@@ -142,14 +142,111 @@ HostWorkList build_work_list(const uint8_t* masks, int n_masks, int H, int F, bo
 
 DeviceWorkList place_work_list(const HostWorkList& hw, void* buf) {
   DeviceWorkList wl;
+  const int32_t* w = static_cast<const int32_t*>(buf);
   wl.buffer = buf;
-  wl.items = static_cast<const int32_t*>(buf);
-  wl.cols = static_cast<const int32_t*>(buf) + hw.off_cols;
-  wl.heavy = static_cast<const int32_t*>(buf) + hw.off_heavy;
+  wl.items = w;
+  wl.cols = w + hw.off_cols;
+  wl.heavy = w + hw.off_heavy;
   wl.n_items = hw.n_items;
   wl.n_heavy = hw.n_heavy;
   wl.n_slots = hw.n_slots;
+  if (hw.wg_per_xcd > 0) {
+    wl.sched_xcd = w + hw.off_xcd;
+    wl.cut_units = w + hw.off_cut_units;
+    wl.n_cut_units = hw.n_cut_units;
+    wl.n_part_slots = hw.n_part_slots;
+    wl.wg_per_xcd = hw.wg_per_xcd;
+  }
   return wl;
+}
+
+void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int T, int P, int F,
+                         int slots_x, bool share_tail) {
+  const int32_t* items = hw.words.data();
+  const int32_t* cols = hw.words.data() + hw.off_cols;
+  const int64_t n_items = hw.n_items;
+  const int tpf = (T + 63) / 64, ptiles = (P + 63) / 64;
+  // Kept tiles of item i for one query block (0 for a query block past its segment).
+  auto tiles_of = [&](int64_t i, int qb) -> int64_t {
+    const int32_t* it = items + 5 * i;
+    const int frame = it[1], beg = it[2], cnt = it[3];
+    const int seg_len = (P > 0 && frame == F) ? P : T;
+    if ((int64_t)qb * rows >= seg_len) return 0;
+    int64_t t = (int64_t)cnt * tpf;
+    if (P > 0 && cnt > 0 && cols[beg + cnt - 1] == F) t += ptiles - tpf;
+    return t;
+  };
+  const int64_t per_b = n_items * nqb, n = (int64_t)B * per_b;
+  auto unit_tiles = [&](int64_t u) { return tiles_of((u % per_b) / nqb, (int)(u % nqb)); };
+  std::vector<int32_t> xcd(4 * 8), pieces, cut_units;
+  int n_part_slots = 0;
+  int64_t wg_max = 0;
+  const int64_t q = n / 8, r = n % 8;
+  for (int x = 0; x < 8; ++x) {
+    const int64_t start = x * q + std::min<int64_t>(x, r), cnt = q + (x < r);
+    int64_t n_dp = cnt;
+    const int64_t first_piece = (int64_t)pieces.size() / 4;
+    // An XCD runs its whole units in rounds of slots_x. If the last round is ragged,
+    // its R units can be cut into k parts each: the parts then take ceil(R k / slots_x)
+    // rounds of 1/k of a unit instead of one round of whole units, and every part
+    // writes its rows' O/l and log-sum-exp (fp32) for a merge pass to read back. The k
+    // of the largest net saving is taken: the time saved (a tile of 64 keys for one
+    // workgroup's query rows takes about 2.8 us at d = 96 and 256 rows, in proportion
+    // to d and the rows) less the partial traffic of all XCDs at about 4 TB/s. A plan
+    // with split frames is left whole: its pieces, dispatched longest first, already
+    // even out the last round, and parts of pieces would add a second merge.
+    const int64_t ragged = cnt % slots_x;
+    if (share_tail && hw.n_heavy == 0 && cnt > slots_x && ragged > 0) {
+      double mean_tiles = 0;
+      for (int64_t u = start + cnt - ragged; u < start + cnt; ++u) mean_tiles += (double)unit_tiles(u);
+      mean_tiles /= (double)ragged;
+      const double tile_s = 2.8e-6 * (rows / 256.0) * (d / 96.0);
+      const double part_s = 8.0 * rows * (d + 4) * 4.0 * 2.0 / 4.0e12;  // per part, all XCDs
+      int best_k = 1;
+      double best = 0.0;
+      for (int kk = 2; kk <= 16; ++kk) {
+        const double rounds = (double)((ragged * kk + slots_x - 1) / slots_x) / kk;
+        const double net = (1.0 - rounds) * mean_tiles * tile_s - (double)(ragged * kk) * part_s;
+        if (net > best) {
+          best = net;
+          best_k = kk;
+        }
+      }
+      if (best_k > 1 && best > 10e-6) {
+        n_dp = cnt - ragged;
+        for (int64_t u = start + n_dp; u < start + cnt; ++u) {
+          const int64_t len = unit_tiles(u);
+          const int parts = (int)std::min<int64_t>(best_k, len);
+          if (parts <= 1) {  // a unit of one tile (or none) runs whole
+            if (len > 0) pieces.insert(pieces.end(), {(int32_t)u, 0, (int32_t)len, -1});
+            continue;
+          }
+          cut_units.insert(cut_units.end(), {(int32_t)u, n_part_slots, parts});
+          for (int p = 0; p < parts; ++p) {
+            const int64_t t0 = len * p / parts, t1 = len * (p + 1) / parts;
+            pieces.insert(pieces.end(), {(int32_t)u, (int32_t)t0, (int32_t)(t1 - t0), n_part_slots++});
+          }
+        }
+      }
+    }
+    const int64_t n_part = (int64_t)pieces.size() / 4 - first_piece;
+    xcd[4 * x] = (int32_t)start;
+    xcd[4 * x + 1] = (int32_t)n_dp;
+    xcd[4 * x + 2] = (int32_t)n_part;
+    xcd[4 * x + 3] = (int32_t)first_piece;
+    wg_max = std::max(wg_max, n_dp + n_part);
+  }
+  hw.n_cut_units = (int)(cut_units.size() / 3);
+  if (pieces.empty()) pieces.assign(4, 0);
+  if (cut_units.empty()) cut_units.assign(3, 0);
+  hw.off_xcd = hw.words.size();
+  hw.words.insert(hw.words.end(), xcd.begin(), xcd.end());
+  hw.off_pieces = hw.words.size();
+  hw.words.insert(hw.words.end(), pieces.begin(), pieces.end());
+  hw.off_cut_units = hw.words.size();
+  hw.words.insert(hw.words.end(), cut_units.begin(), cut_units.end());
+  hw.n_part_slots = n_part_slots;
+  hw.wg_per_xcd = (int)wg_max;
 }
 
 // A cached plan: its device buffer and, per stream that enqueued work with it, an
@@ -192,19 +289,31 @@ struct PlanUse {
 
 // Returns the device-resident work list for H heads with n_masks masks (1: shared,
 // H: one per head), split or not, uploading it on first use on device dev.
+// The forward launch a plan is scheduled for (append_fwd_schedule).
+struct FwdLaunch {
+  int B, nqb, rows, d, T, P, F, slots_x;
+  bool share_tail;
+};
+
 int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_split, int dev,
-                  PlanUse* out) {
+                  PlanUse* out, const FwdLaunch* fl = nullptr) {
   std::string key(reinterpret_cast<const char*>(masks), (size_t)n_masks * F * F);
   key += allow_split ? "|s|" : "|u|";
   key += std::to_string(H) + "|" + std::to_string(n_masks) + "|" + std::to_string(F) + "|" +
          std::to_string(dev);
+  if (fl)
+    for (int v : {fl->B, fl->nqb, fl->rows, fl->d, fl->T, fl->P, fl->F, fl->slots_x, (int)fl->share_tail})
+      key += "|" + std::to_string(v);
   std::lock_guard<std::mutex> lock(g_cache_mutex);
   if (auto h = g_cache.acquire(key)) {
     out->wl = h->value.wl;
     out->slot = h;
     return TA_OK;
   }
-  const HostWorkList hw = build_work_list(masks, n_masks, H, F, allow_split);
+  HostWorkList hw = build_work_list(masks, n_masks, H, F, allow_split);
+  if (fl)
+    append_fwd_schedule(hw, fl->B, fl->nqb, fl->rows, fl->d, fl->T, fl->P, fl->F, fl->slots_x,
+                        fl->share_tail);
   const size_t total = hw.words.size() * sizeof(int32_t);
   void* buf = nullptr;
   hipError_t e = hipMalloc(&buf, total);
@@ -262,6 +371,22 @@ struct PlanGuard {
   explicit PlanGuard(void* s) : stream(s) {}
   ~PlanGuard() { end_plan_use(use, stream); }
 };
+
+int resident_slots_per_xcd(int dev) {
+  static std::mutex mu;
+  static std::map<int, int> slots;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = slots.find(dev);
+  if (it == slots.end()) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 8) {
+      (void)hipGetLastError();
+      cus = 256;  // MI355X
+    }
+    it = slots.emplace(dev, 2 * (cus / 8)).first;  // two forward workgroups per compute unit
+  }
+  return it->second;
+}
 
 // Partial-result workspace of split frames, one per (device, stream) so that calls
 // on different streams never share it; replaced by a larger one on demand, every
@@ -353,8 +478,15 @@ int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, i
   a.items = wl->items;
   a.cols = wl->cols;
   a.n_items = wl->n_items;
+  // ws: [frame pieces' O/l][their lse][parts of units: O/l and lse per row]
+  const size_t frame_rows = (size_t)wl->n_slots * B * L;
   a.ws_o = ws;
-  a.ws_lse = ws ? ws + (size_t)wl->n_slots * B * L * d : nullptr;
+  a.ws_lse = ws ? ws + frame_rows * d : nullptr;
+  a.ws_parts = ws ? ws + frame_rows * (d + 1) : nullptr;
+  a.sched = wl->sched_xcd;
+  a.cut_units = wl->cut_units;
+  a.n_cut_units = wl->n_cut_units;
+  a.wg_per_xcd = wl->wg_per_xcd;
   a.lse = lse;
   // Logits are formed from |scale| (a negative scale flips the sign of q, which
   // is exact in bf16). scale == 0 zeroes q instead, so every logit is exactly 0
@@ -368,7 +500,10 @@ int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, i
     a.qflip = std::signbit(scale) ? 0x80008000u : 0u;
     a.qmask = 0xFFFFFFFFu;
   }
-  a.n_wg = (uint32_t)((int64_t)B * wl->n_items * nqb);
+  if (wl->wg_per_xcd == 0) {  // nothing to run (no query block has rows)
+    g_last_error.clear();
+    return TA_OK;
+  }
   e = ta::launch_tile_attn_fwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("kernel launch: ") + hipGetErrorString(e));
   if (wl->n_heavy > 0) {
@@ -412,20 +547,25 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
           aug[((size_t)m * n_seg + i) * n_seg + j] = masks[((size_t)m * F + i) * F + j] ? 1 : 0;
     masks = aug.data();
   }
+  const int rows = ta::fwd_rows_per_workgroup(d);
+  const FwdLaunch fl{B, (int)nqb, rows, d, T, P, F, resident_slots_per_xcd(dev), true};
   PlanGuard plan(stream);
-  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &plan.use);
+  int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &plan.use, &fl);
   if (st != TA_OK) return st;
   const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
-  if ((size_t)plan.use.wl.n_slots * B * L * (d + 1) * sizeof(float) > kMaxWorkspaceBytes ||
-      (int64_t)B * plan.use.wl.n_items * nqb > max_wg) {
+  auto ws_bytes = [&](const DeviceWorkList& w) {
+    return ((size_t)w.n_slots * B * L * (d + 1) + (size_t)w.n_part_slots * rows * (d + 4)) * sizeof(float);
+  };
+  if (ws_bytes(plan.use.wl) > kMaxWorkspaceBytes || (int64_t)8 * plan.use.wl.wg_per_xcd > max_wg) {
     end_plan_use(plan.use, stream);
-    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &plan.use);  // the same rows, not split
+    const FwdLaunch plain{B, (int)nqb, rows, d, T, P, F, fl.slots_x, false};
+    st = work_list_for(masks, n_masks, H, n_seg, false, dev, &plan.use, &plain);  // the same rows, not split
     if (st != TA_OK) return st;
   }
   const DeviceWorkList* wl = &plan.use.wl;
   void* ws = nullptr;
-  if (wl->n_slots > 0) {
-    st = workspace_for(dev, stream, (size_t)wl->n_slots * B * L * (d + 1) * sizeof(float), &ws);
+  if (ws_bytes(*wl) > 0) {
+    st = workspace_for(dev, stream, ws_bytes(*wl), &ws);
     if (st != TA_OK) return st;
   }
   st = enqueue_fwd(q, k, v, out, B, H, F, T, d, P, *wl, static_cast<float*>(ws), scale, lse, stream);

@@ -285,21 +285,24 @@ struct FwdItem {
   uint16_t* Oh;
   const int32_t* cols;
   size_t head_rows;
-  uint32_t b, bh, per_b, n_wg;
+  uint32_t b, bh, B;
   int frame, kbeg, n_kept, slot, qb, seg0, seg_len;
+  // Tiles of the kept list this workgroup takes: [t0, t0 + nt), nt < 0 for all of
+  // them; a part of the list (part >= 0) writes its rows to block `part` of ws_parts.
+  int t0, nt, part;
 };
 
 // The rows of one workgroup with QB 32-query column blocks per wave. The grid's
 // query blocks hold fwd_rows_per_wg<D>() rows whatever QB is: at d = 64 a block at the
 // end of a segment with at most 32 valid rows per wave runs with QB = 1, so no wave
 // computes a column block that lies wholly past the segment end.
-template <int D, bool PREFIX, int QB>
+template <int D, bool PREFIX, int QB, bool PARTS>
 __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>& lay,
                                          uint16_t (&sK)[2][Shape<D>::kTileElems],
                                          uint16_t (&sV)[2][Shape<D>::kTileElems],
                                          float* __restrict__ ws_o, float* __restrict__ ws_lse,
-                                         float* __restrict__ lse, float c, uint32_t qflip,
-                                         uint32_t qmask) {
+                                         float* __restrict__ lse, float* __restrict__ ws_parts, float c,
+                                         uint32_t qflip, uint32_t qmask) {
   using Sh = Shape<D>;
   constexpr int kWaveQ = 32 * QB;
   constexpr int kBlockQ = fwd_rows_per_wg<D>();
@@ -309,8 +312,9 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
   uint16_t* Oh = it.Oh;
   const int32_t* cols = it.cols;
   const size_t head_rows = it.head_rows;
-  const uint32_t b = it.b, bh = it.bh, per_b = it.per_b, n_wg = it.n_wg;
+  const uint32_t b = it.b, bh = it.bh;
   const int kbeg = it.kbeg, n_kept = it.n_kept, slot = it.slot, qb = it.qb;
+  const int part = PARTS ? it.part : -1;
   const int seg0 = it.seg0, seg_len = it.seg_len;
   [[maybe_unused]] const int F = lay.F, T = lay.T, P = lay.P;
 
@@ -357,6 +361,9 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
     // the text segment (index F) sorts last in a kept list
     if (n_kept > 0 && cols[kbeg + n_kept - 1] == F) n_tiles += (P + kBlockK - 1) / kBlockK - tpf;
   }
+  if constexpr (PARTS) {
+    if (it.nt >= 0) n_tiles = it.nt;  // a part of the kept tiles, from tile it.t0
+  }
 
   if (n_tiles > 0) {
     TileLoader<D, true> kl;
@@ -369,6 +376,9 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
     va.init(lane);
     SegmentCursor<PREFIX> cur, nxt;  // tile t (being consumed) and tile t+1 (being loaded)
     cur.start(cols + kbeg, lay);
+    if constexpr (PARTS) {
+      if (it.t0 > 0) cur.skip(it.t0, n_kept);
+    }
     kl.load(Kh, cur.key0(), cur.nvalid(), sK[0], wave);
     vl.load(Vh, cur.key0(), cur.nvalid(), sV[0], wave);
     nxt = cur;
@@ -557,7 +567,7 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
     const int qrow = qrow0_e + 32 * qs;
     if (qrow < seg_len) {
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      if (slot < 0) {
+      if (slot < 0 && part < 0) {
         uint16_t* op = Oh + ((size_t)seg0 + qrow) * D;
 #pragma unroll
         for (int mb = 0; mb < Sh::kDBlocks; ++mb)
@@ -573,10 +583,13 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
               l_tot > 0.f ? (m_ref[qs] * c + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f
                           : -INFINITY;
       } else {
-        const uint32_t nb = n_wg / per_b;  // batch size
+        // A part of the kept tiles (part >= 0) goes to its own slot of kBlockQ rows of
+        // D + 4 floats (O/l, then the log-sum-exp), a piece of a split frame (slot >= 0)
+        // to the frame's partial rows.
         const int slot_rows = PREFIX ? max(T, P) : T;  // rows per (slot, batch entry)
-        const size_t prow = ((size_t)slot * nb + b) * slot_rows + qrow;
-        float* op = ws_o + prow * D;
+        const size_t prow = part >= 0 ? (size_t)part * kBlockQ + (qrow - qb * kBlockQ)
+                                    : ((size_t)slot * it.B + b) * slot_rows + qrow;
+        float* op = part >= 0 ? ws_parts + prow * (D + 4) : ws_o + prow * D;
 #pragma unroll
         for (int mb = 0; mb < Sh::kDBlocks; ++mb)
 #pragma unroll
@@ -585,61 +598,159 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
                              o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
             *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * i + 4 * hf_e) = x;
           }
-        if (hf_e == 0) ws_lse[prow] = m_ref[qs] * c + __builtin_amdgcn_logf(l_tot);
+        if (hf_e == 0) *(part >= 0 ? op + D : ws_lse + prow) = m_ref[qs] * c + __builtin_amdgcn_logf(l_tot);
       }
     }
   }
 }
 
-template <int D, bool PREFIX>
+// Work of one launch. Logical unit u = (batch entry b, item i, query block qb), qb
+// fastest, covers the item's kept tiles for kBlockQ query rows. XCD x (the workgroups
+// with blockIdx % 8 == x; each XCD has its own L2) runs, in order, the units
+// [start_x, start_x + n_dp_x) one per workgroup, then n_part_x workgroups that each take
+// one part of a unit that would otherwise run in a ragged last round of whole units:
+// a piece {u, first tile, tiles, partial slot}. sched holds {start_x, n_dp_x, n_part_x,
+// first piece} per XCD, then the pieces. Launches without parts (PARTS false) take the
+// whole units of each XCD from the same contiguous shares, computed in place.
+
+template <int D, bool PREFIX, bool PARTS>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int H,
-    int F, int T, int P, int nqb, uint32_t n_wg, float* __restrict__ ws_o,
-    float* __restrict__ ws_lse, float* __restrict__ lse, float c, uint32_t qflip, uint32_t qmask) {
+    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int B,
+    int H, int F, int T, int P, int nqb, const int32_t* __restrict__ sched,
+    float* __restrict__ ws_o, float* __restrict__ ws_lse, float* __restrict__ lse,
+    float* __restrict__ ws_parts, float c, uint32_t qflip, uint32_t qmask) {
   using Sh = Shape<D>;
   constexpr int kBlockQ = fwd_rows_per_wg<D>();
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
   __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
 
+  const uint32_t x = blockIdx.x % 8, pos = blockIdx.x / 8;
+  const uint32_t per_b = (uint32_t)n_items * (uint32_t)nqb;
   FwdItem it;
-  const uint32_t work = xcd_remap(blockIdx.x, n_wg);
-  it.n_wg = n_wg;
-  it.per_b = (uint32_t)n_items * (uint32_t)nqb;
-  it.b = work / it.per_b;
-  const uint32_t rem = work - it.b * it.per_b;
-  const int32_t* item = items + 5 * (rem / nqb);
-  it.bh = it.b * (uint32_t)H + (uint32_t)item[0];
-  it.frame = item[1];
-  it.kbeg = item[2];
-  it.n_kept = item[3];
-  it.slot = item[4];  // >= 0: a piece of a split frame, written as a partial
-  it.qb = (int)(rem % nqb);
-  it.cols = cols;
-  const Layout<PREFIX> lay{F, T, P};
-  it.seg0 = lay.start(it.frame);
-  it.seg_len = lay.len(it.frame);
-  // With a prefix the text segment is shorter than the grid's query blocks assume.
-  if (PREFIX && it.qb * kBlockQ >= it.seg_len) return;
-
-  it.head_rows = (size_t)P * PREFIX + (size_t)F * T;
-  const size_t head_elems = it.head_rows * D;
-  it.Qh = Q + it.bh * head_elems;
-  it.Kh = K + it.bh * head_elems;
-  it.Vh = V + it.bh * head_elems;
-  it.Oh = O + it.bh * head_elems;
-
-  // A query block at the end of a segment with at most 32 valid rows per wave runs with
-  // one column block per wave. Only at d = 64: at d = 96 the second instance of the
-  // tile loop makes the register allocator spill the main one.
-  if constexpr (fwd_q_blocks<D>() == 2 && D == 64) {
-    if (it.seg_len - it.qb * kBlockQ <= kWaves * 32) {
-      fwd_rows<D, PREFIX, 1>(it, lay, sK, sV, ws_o, ws_lse, lse, c, qflip, qmask);
-      return;
+  it.t0 = 0;
+  it.nt = -1;
+  it.part = -1;
+  uint32_t u;
+  if constexpr (!PARTS) {
+    // Without parts the schedule gives XCD x the contiguous units [x q + min(x, r), + q +
+    // (x < r)) of the n = q 8 + r units, which need no table lookup.
+    const uint32_t n = (uint32_t)B * per_b, q = n / 8, r = n % 8;
+    if (pos >= q + (x < r ? 1u : 0u)) return;
+    u = x * q + min(x, r) + pos;
+  } else {
+    const int32_t* xi = sched + 4 * x;
+    const int n_dp = xi[1];
+    if ((int)pos < n_dp) {
+      u = (uint32_t)xi[0] + pos;
+    } else {
+      if ((int)pos >= n_dp + xi[2]) return;
+      const int32_t* pc = sched + 32 + 4 * (xi[3] + (int)pos - n_dp);
+      u = (uint32_t)pc[0];
+      it.t0 = pc[1];
+      it.nt = pc[2];
+      it.part = pc[3];
     }
   }
-  fwd_rows<D, PREFIX, fwd_q_blocks<D>()>(it, lay, sK, sV, ws_o, ws_lse, lse, c, qflip, qmask);
+  const Layout<PREFIX> lay{F, T, P};
+  {
+    it.B = (uint32_t)B;
+    it.b = u / per_b;
+    const uint32_t rem = u - it.b * per_b;
+    const int32_t* item = items + 5 * (rem / nqb);
+    it.bh = it.b * (uint32_t)H + (uint32_t)item[0];
+    it.frame = item[1];
+    it.kbeg = item[2];
+    it.n_kept = item[3];
+    it.slot = item[4];  // >= 0: a piece of a split frame, written as a partial
+    it.qb = (int)(rem % nqb);
+    it.cols = cols;
+    it.seg0 = lay.start(it.frame);
+    it.seg_len = lay.len(it.frame);
+    // With a prefix the text segment is shorter than the grid's query blocks assume.
+    if (PREFIX && it.qb * kBlockQ >= it.seg_len) return;
+
+    it.head_rows = (size_t)P * PREFIX + (size_t)F * T;
+    const size_t head_elems = it.head_rows * D;
+    it.Qh = Q + it.bh * head_elems;
+    it.Kh = K + it.bh * head_elems;
+    it.Vh = V + it.bh * head_elems;
+    it.Oh = O + it.bh * head_elems;
+
+    // A query block at the end of a segment with at most 32 valid rows per wave runs
+    // with one column block per wave. Only at d = 64: at d = 96 the second instance of
+    // the tile loop makes the register allocator spill the main one.
+    if constexpr (fwd_q_blocks<D>() == 2 && D == 64) {
+      if (it.seg_len - it.qb * kBlockQ <= kWaves * 32) {
+        fwd_rows<D, PREFIX, 1, PARTS>(it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip, qmask);
+        return;
+      }
+    }
+    fwd_rows<D, PREFIX, fwd_q_blocks<D>(), PARTS>(it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip,
+                                                  qmask);
+  }
+}
+
+// Combines the parts of query blocks whose kept tiles were shared out among several
+// workgroups (the end of each XCD's run); a part's row is D + 4 floats, O/l then its
+// log-sum-exp. One thread per (split unit, row of the block, 8 consecutive d): with
+// M the largest part log-sum-exp (base 2), O = sum_p
+// 2^(lse_p - M) (O/l)_p / sum_p 2^(lse_p - M). A unit of an item that is itself a
+// piece of a split frame (item slot >= 0) writes the frame piece's partial row
+// (fp32 O/l and base-2 log-sum-exp) for the frame merge; any other writes its output
+// row in bf16 (RNE) and the natural-log log-sum-exp.
+template <int D>
+__global__ __launch_bounds__(256) void merge_parts_kernel(
+    const float* __restrict__ ws_parts, const int32_t* __restrict__ cut_units, int n_units,
+    const int32_t* __restrict__ items,
+    int n_items, int nqb, int rows_per_block, int B, int H, int F, int T, int P,
+    uint16_t* __restrict__ O, float* __restrict__ lse, float* __restrict__ ws_o,
+    float* __restrict__ ws_lse) {
+  constexpr int kGroups = D / 8;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t per_unit = (size_t)rows_per_block * kGroups;
+  if (idx >= per_unit * (size_t)n_units) return;
+  const int un = (int)(idx / per_unit);
+  const int r = (int)((idx % per_unit) / kGroups), grp = (int)(idx % kGroups);
+  const uint32_t u = (uint32_t)cut_units[3 * un];
+  const int slot0 = cut_units[3 * un + 1], np = cut_units[3 * un + 2];
+  const uint32_t per_b = (uint32_t)n_items * (uint32_t)nqb;
+  const uint32_t b = u / per_b, rem = u - b * per_b;
+  const int32_t* item = items + 5 * (rem / nqb);
+  const int head = item[0], frame = item[1], slot = item[4];
+  const int qrow = (int)(rem % nqb) * rows_per_block + r;
+  const int seg0 = frame < F ? P + frame * T : 0, seg_len = frame < F ? T : P;
+  if (qrow >= seg_len) return;
+  float mx = -INFINITY;
+  for (int p = 0; p < np; ++p) mx = fmaxf(mx, ws_parts[((size_t)(slot0 + p) * rows_per_block + r) * (D + 4) + D]);
+  f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+  float wsum = 0.f;
+  if (mx != -INFINITY) {
+    for (int p = 0; p < np; ++p) {
+      const float* row = ws_parts + ((size_t)(slot0 + p) * rows_per_block + r) * (D + 4);
+      const float w = fast_exp2(row[D] - mx);
+      const f32x4* src = reinterpret_cast<const f32x4*>(row + 8 * grp);
+      a0 += w * src[0];
+      a1 += w * src[1];
+      wsum += w;
+    }
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  const f32x8 x = {a0[0] * inv, a0[1] * inv, a0[2] * inv, a0[3] * inv,
+                   a1[0] * inv, a1[1] * inv, a1[2] * inv, a1[3] * inv};
+  const float lse2 = wsum > 0.f ? mx + __builtin_amdgcn_logf(wsum) : -INFINITY;
+  if (slot < 0) {
+    const size_t orow = (b * H + head) * ((size_t)P + (size_t)F * T) + seg0 + qrow;
+    *reinterpret_cast<bf16x8*>(O + orow * D + 8 * grp) = __builtin_convertvector(x, bf16x8);
+    if (lse && grp == 0) lse[orow] = lse2 * 0.69314718055994531f;
+  } else {
+    const size_t prow = ((size_t)slot * B + b) * (size_t)max(T, P) + qrow;
+    f32x4* dst = reinterpret_cast<f32x4*>(ws_o + prow * D + 8 * grp);
+    dst[0] = f32x4{x[0], x[1], x[2], x[3]};
+    dst[1] = f32x4{x[4], x[5], x[6], x[7]};
+    if (grp == 0) ws_lse[prow] = lse2;
+  }
 }
 
 // Combines the pieces of split query frames (or of the split text segment of the
@@ -691,14 +802,29 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(
 template <int D>
 hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
   const int nqb = (std::max(a.T, a.P) + fwd_rows_per_wg<D>() - 1) / fwd_rows_per_wg<D>();
-  if (a.P > 0)
-    hipLaunchKernelGGL((tile_attn_fwd_kernel<D, true>), dim3(a.n_wg), dim3(kThreads), 0, stream, a.q,
-                       a.k, a.v, a.out, a.items, a.cols, a.n_items, a.H, a.F, a.T, a.P, nqb, a.n_wg,
-                       a.ws_o, a.ws_lse, a.lse, a.c, a.qflip, a.qmask);
-  else
-    hipLaunchKernelGGL((tile_attn_fwd_kernel<D, false>), dim3(a.n_wg), dim3(kThreads), 0, stream,
-                       a.q, a.k, a.v, a.out, a.items, a.cols, a.n_items, a.H, a.F, a.T, 0, nqb,
-                       a.n_wg, a.ws_o, a.ws_lse, a.lse, a.c, a.qflip, a.qmask);
+  const dim3 grid(8u * (uint32_t)a.wg_per_xcd);
+  // The kernel that can run parts of units only where the schedule has some.
+  auto go = [&](auto prefix, auto parts) {
+    constexpr bool kPrefix = decltype(prefix)::value, kParts = decltype(parts)::value;
+    hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kParts>), grid, dim3(kThreads), 0, stream, a.q,
+                       a.k, a.v, a.out, a.items, a.cols, a.n_items, a.B, a.H, a.F, a.T, kPrefix ? a.P : 0,
+                       nqb, a.sched, a.ws_o, a.ws_lse, a.lse, a.ws_parts, a.c, a.qflip, a.qmask);
+  };
+  using Y = std::true_type;
+  using N = std::false_type;
+  if (a.P > 0) {
+    if (a.n_cut_units > 0) go(Y{}, Y{});
+    else go(Y{}, N{});
+  } else {
+    if (a.n_cut_units > 0) go(N{}, Y{});
+    else go(N{}, N{});
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_cut_units == 0) return e;
+  const size_t threads = (size_t)a.n_cut_units * fwd_rows_per_wg<D>() * (D / 8);
+  hipLaunchKernelGGL(merge_parts_kernel<D>, dim3((uint32_t)((threads + 255) / 256)), dim3(256), 0, stream,
+                     a.ws_parts, a.cut_units, a.n_cut_units, a.items, a.n_items, nqb,
+                     fwd_rows_per_wg<D>(), a.B, a.H, a.F, a.T, a.P, a.out, a.lse, a.ws_o, a.ws_lse);
   return hipGetLastError();
 }
 

@@ -83,15 +83,19 @@ extern "C" int tile_attn_fwd_heads_noalloc(const void* q, const void* k, const v
   // fit the scratch array, otherwise every frame in one piece (no partials).
   const int64_t nqb = (T + ta::fwd_rows_per_workgroup(d) - 1) / ta::fwd_rows_per_workgroup(d);
   const int64_t max_wg = (int64_t)UINT32_MAX / ta::kThreads;
+  // Every unit runs whole (no shared-out tail): the partials stay those of split frames.
+  const int rows = ta::fwd_rows_per_workgroup(d);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  const int slots_x = e == hipSuccess ? resident_slots_per_xcd(dev) : 64;
   HostWorkList hw = build_work_list(tile_masks, n_masks, H, F, true);
   if ((size_t)hw.n_slots * B * T * (d + 1) > kPartialFloats || (int64_t)B * hw.n_items * nqb > max_wg)
     hw = build_work_list(tile_masks, n_masks, H, F, false);
+  append_fwd_schedule(hw, B, (int)nqb, rows, d, T, 0, F, slots_x, false);
   if (hw.words.size() > kPlanWords)
     return fail(TA_ERR_BAD_SHAPE, "the work plan needs " + std::to_string(hw.words.size()) +
                                       " words, more than the " + std::to_string(kPlanWords) +
                                       " of tile_attn_fwd_heads_noalloc's static scratch");
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
   int32_t* base = nullptr;
   if ((st = scratch_on(dev, &base)) != TA_OK) return st;

@@ -89,6 +89,16 @@ struct SegmentCursor {
       }
     }
   }
+  // Moves on by n tiles (n >= 0 and within the list).
+  __device__ __forceinline__ void skip(int n, int n_segments) {
+    while (n >= tiles - kt && e + 1 < n_segments) {
+      n -= tiles - kt;
+      kt = 0;
+      kf = cols[++e];
+      tiles = (L.len(kf) + kBlockK - 1) / kBlockK;
+    }
+    kt += n;
+  }
   __device__ __forceinline__ size_t key0() const { return (size_t)L.start(kf) + kt * kBlockK; }
   __device__ __forceinline__ int nvalid() const { return min(kBlockK, L.len(kf) - kt * kBlockK); }
 };

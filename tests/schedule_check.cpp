@@ -1,0 +1,98 @@
+// Host-only check of the forward launch schedule (append_fwd_schedule in
+// paper_2502_06155_amd/csrc/tile_attn_host.cpp), linked against the built library and
+// run by tests/test_schedule.py: for each shape, every (unit, kept tile) is covered
+// exactly once by the whole units and the parts of the schedule, every partial slot
+// belongs to one unit, and the per-XCD workgroup counts fit the grid. Prints one line
+// per shape: "<name> units U whole W parts P slots S".
+#include <cstdio>
+#include <cstdlib>
+#include <map>
+#include <vector>
+
+#include "host_internal.h"
+#include "tile_attn.h"
+
+using namespace ta::host;
+
+namespace {
+
+int check(const char* name, int B, int H, int F, int T, int P, int d, int g, int form) {
+  const int rows = d == 128 ? 128 : 256, slots_x = 64;
+  std::vector<uint8_t> m((size_t)F * F);
+  tile_attn_make_mask(F, g, form, m.data());
+  int n_seg = F;
+  std::vector<uint8_t> aug;
+  if (P > 0) {  // the text row and column are kept entirely
+    n_seg = F + 1;
+    aug.assign((size_t)n_seg * n_seg, 1);
+    for (int i = 0; i < F; ++i)
+      for (int j = 0; j < F; ++j) aug[i * n_seg + j] = m[i * F + j];
+  }
+  HostWorkList hw = build_work_list(P > 0 ? aug.data() : m.data(), 1, H, n_seg, true);
+  const int L = T > P ? T : P, nqb = (L + rows - 1) / rows;
+  append_fwd_schedule(hw, B, nqb, rows, d, T, P, F, slots_x, true);
+  const int32_t* w = hw.words.data();
+  const int32_t* items = w;
+  const int32_t* cols = w + hw.off_cols;
+  const int32_t* xcd = w + hw.off_xcd;
+  const int32_t* pieces = w + hw.off_pieces;
+  const int32_t* cut = w + hw.off_cut_units;
+  if (hw.off_pieces != hw.off_xcd + 32) return std::printf("%s: pieces do not follow the XCD table\n", name), 1;
+  const long per_b = (long)hw.n_items * nqb, n = B * per_b;
+  const int tpf = (T + 63) / 64, ptiles = (P + 63) / 64;
+  auto tiles = [&](long u) -> long {
+    const int32_t* it = items + 5 * ((u % per_b) / nqb);
+    const int qb = (int)(u % nqb), frame = it[1], beg = it[2], cnt = it[3];
+    const int seg_len = (P > 0 && frame == F) ? P : T;
+    if ((long)qb * rows >= seg_len) return 0;
+    long t = (long)cnt * tpf;
+    if (P > 0 && cnt > 0 && cols[beg + cnt - 1] == F) t += ptiles - tpf;
+    return t;
+  };
+  std::vector<long> covered(n, 0);
+  std::map<int, int> slot_unit;
+  long whole = 0, parts = 0;
+  for (int x = 0; x < 8; ++x) {
+    if (xcd[4 * x + 1] + xcd[4 * x + 2] > hw.wg_per_xcd) return std::printf("%s: grid too small\n", name), 1;
+    for (int p = 0; p < xcd[4 * x + 1]; ++p) covered[xcd[4 * x] + p] += tiles(xcd[4 * x] + p);
+    whole += xcd[4 * x + 1];
+    for (int p = 0; p < xcd[4 * x + 2]; ++p) {
+      const int32_t* pc = pieces + 4 * (xcd[4 * x + 3] + p);
+      if (pc[1] < 0 || pc[2] <= 0 || pc[1] + pc[2] > tiles(pc[0])) return std::printf("%s: bad part\n", name), 1;
+      covered[pc[0]] += pc[2];
+      ++parts;
+      if (pc[3] >= 0 && !slot_unit.emplace(pc[3], pc[0]).second) return std::printf("%s: slot reused\n", name), 1;
+    }
+  }
+  for (long u = 0; u < n; ++u)
+    if (covered[u] != tiles(u)) return std::printf("%s: unit %ld covers %ld of %ld tiles\n", name, u, covered[u], tiles(u)), 1;
+  int slots = 0;
+  for (int k = 0; k < hw.n_cut_units; ++k)
+    for (int s = cut[3 * k + 1]; s < cut[3 * k + 1] + cut[3 * k + 2]; ++s, ++slots)
+      if (slot_unit.count(s) == 0 || slot_unit[s] != cut[3 * k]) return std::printf("%s: slot of another unit\n", name), 1;
+  if (slots != hw.n_part_slots || (int)slot_unit.size() != hw.n_part_slots) return std::printf("%s: slot count\n", name), 1;
+  std::printf("%s units %ld whole %ld parts %ld slots %d\n", name, n, whole, parts, hw.n_part_slots);
+  return 0;
+}
+
+}  // namespace
+
+int main() {
+  int bad = 0;
+  bad |= check("93f-col", 1, 24, 24, 3600, 0, 96, 1, TA_MASK_COL);
+  bad |= check("29f-col", 1, 24, 8, 3600, 0, 96, 1, TA_MASK_COL);
+  bad |= check("sp-col", 1, 6, 24, 3600, 0, 96, 1, TA_MASK_COL);
+  bad |= check("sp-sym", 1, 6, 24, 3600, 0, 96, 1, TA_MASK_SYM);
+  bad |= check("long-col", 1, 24, 48, 1200, 0, 96, 2, TA_MASK_COL);
+  bad |= check("d128-sym", 1, 18, 24, 3600, 0, 128, 1, TA_MASK_SYM);
+  bad |= check("cog-sym", 1, 48, 13, 1350, 226, 64, 1, TA_MASK_SYM);
+  bad |= check("batch3", 3, 5, 7, 333, 0, 96, 2, TA_MASK_SYM);
+  // the shapes of test_ragged_round_in_parts (tests/test_gpu_parity.py, and gpu-e in
+  // tests/test_gpu_mmdit.py)
+  bad |= check("gpu-a", 1, 16, 17, 500, 0, 64, 1, TA_MASK_COL);
+  bad |= check("gpu-b", 1, 12, 20, 700, 0, 96, 2, TA_MASK_COL);
+  bad |= check("gpu-c", 1, 32, 6, 700, 0, 96, 1, TA_MASK_SYM);
+  bad |= check("gpu-d", 1, 8, 11, 700, 0, 128, 1, TA_MASK_COL);
+  bad |= check("gpu-e", 1, 12, 9, 1350, 226, 64, 1, TA_MASK_SYM);
+  return bad;
+}

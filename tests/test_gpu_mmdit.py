@@ -131,3 +131,29 @@ def test_mmdit_cog_shape_sampled(k):
     hh = 17
     ref_lse = ommd.attention_mmdit_lse(qb[:, hh:hh + 1], kb[:, hh:hh + 1], mask, w.T, w.prefix, w.scale())
     assert_lse(lse[:, hh:hh + 1], ref_lse, f"cog-k{k}-lse")
+
+
+def test_mmdit_ragged_round_in_parts():
+    """An MM-DiT launch (12 heads of 64, 9 frames x 1350 tokens, 226 text tokens, sym
+    g=1) whose XCDs end on a ragged round: that round's query blocks, text blocks
+    included, run in parts over their kept tiles (tests/test_schedule.py confirms the
+    cut). Every text row and sampled video rows of two heads, and their log-sum-exp."""
+    B, H, F, T, P, d = 1, 12, 9, 1350, 226, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=P + F, prefix=P)
+    mask = om.tile_mask(F, 1, "sym")
+    scale = d ** -0.5
+    print(f"[case] mmdit parts H={H} F={F} T={T} P={P} d={d}", flush=True)
+    got, lse = run_mmdit(qb, kb, vb, mask, T, P, scale)
+    rng = np.random.default_rng(F)
+    rows = []
+    for h in (0, H - 1):
+        rows += [(0, h, s) for s in range(P)]
+        for f in range(F):
+            for r in {0, T - 1, 1279, int(rng.integers(0, T))}:
+                rows.append((0, h, P + f * T + r))
+    b, h, s = (np.array(x) for x in zip(*rows))
+    ref = ommd.attention_mmdit_rows(qb, kb, vb, mask, T, P, scale, b, h, s)
+    assert_parity(got[b, h, s], ref, "mmdit-parts")
+    for hh in (0, H - 1):
+        ref_lse = ommd.attention_mmdit_lse(qb[:, hh:hh + 1], kb[:, hh:hh + 1], mask, T, P, scale)
+        assert_lse(lse[:, hh:hh + 1], ref_lse, f"mmdit-parts-lse-h{hh}")

@@ -452,3 +452,33 @@ def test_max_frames():
     mask[::97, :] = 1
     mask[5::211, :] = 0
     full_check(qb, kb, vb, mask, T, d ** -0.5, "max-frames")
+
+
+# ---- the ragged last round of an XCD run in parts over the kept tiles ----------------
+
+PART_CASES = [  # (B, H, F, T, d, g, form): each XCD's last round is cut into parts
+    (1, 16, 17, 500, 64, 1, "col"),
+    (1, 12, 20, 700, 96, 2, "col"),
+    (1, 32, 6, 700, 96, 1, "sym"),
+    (1, 8, 11, 700, 128, 1, "col"),
+]
+
+
+@pytest.mark.parametrize("B,H,F,T,d,g,form", PART_CASES)
+def test_ragged_round_in_parts(B, H, F, T, d, g, form):
+    """Launches whose XCDs would end on a ragged round of whole query blocks run that
+    round's blocks in parts over the kept tiles (merged by log-sum-exp; the host check
+    in tests/test_schedule.py confirms these shapes are cut). Sampled rows of every
+    frame and head, and the log-sum-exp of two heads, against the oracle."""
+    print(f"[case] parts B={B} H={H} F={F} T={T} d={d} {form} g={g}", flush=True)
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=F * T + d)
+    mask = om.tile_mask(F, g, form)
+    scale = d ** -0.5
+    got, lse = run_gpu_heads(qb, kb, vb, mask, T, scale)
+    b, h, s = sample_rows(B, H, F, T, per_frame=6, seed=T)
+    assert_parity(got[b, h, s], oa.attention_rows(qb, kb, vb, mask, T, scale, b, h, s), "parts")
+    for hh in (0, H - 1):
+        ref = oa.attention_lse(qb[:, hh:hh + 1], kb[:, hh:hh + 1], mask, T, scale)
+        assert_lse(lse[:, hh:hh + 1], ref, f"parts-lse-h{hh}")
+    # the plain entry point takes the same schedule: same bits
+    assert np.array_equal(run_gpu(qb, kb, vb, mask, T, scale), got)
