@@ -66,12 +66,18 @@ HostWorkList build_work_list(const uint8_t* masks, int n_masks, int H, int F, bo
 // The device view of hw's words placed at buf.
 DeviceWorkList place_work_list(const HostWorkList& hw, void* buf);
 
-// Enqueues the forward kernel (and the merge of split frames) on stream for a plan
-// already resident on the device; ws holds n_slots * B * max(T, P) * (d + 1) floats
-// (unused when the plan has no slots).
+// Enqueues the forward kernel (and the merges of split frames and of parts) on stream
+// for a plan already resident on the device; ws holds n_slots * B * max(T, P) * (d + 1)
+// floats, then n_part_slots * rows * (d + 4) (unused when the plan has neither). queue:
+// null for one workgroup per unit, else 9 int32 on the device, zero, that the kernel's
+// persistent work loop (d = 64) uses and leaves zero; launches that may run at the same
+// time need different queues. slots_x: resident workgroups per XCD.
 int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
                 int T, int d, int P, const DeviceWorkList& plan, float* ws, float scale,
-                float* lse, void* stream);
+                float* lse, void* stream, int* queue, int slots_x);
+
+// The forward queue counters of (dev, stream): allocated and zeroed on first use.
+int queue_for(int dev, void* stream, int** out);
 
 }  // namespace host
 }  // namespace ta

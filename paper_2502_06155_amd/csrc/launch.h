@@ -41,7 +41,12 @@ struct FwdArgs {
   const int32_t* sched;
   const int32_t* cut_units;
   int n_cut_units;
-  int wg_per_xcd;       // workgroups per XCD (the grid is 8 times that)
+  int wg_per_xcd;       // queue positions of the busiest XCD
+  int slots_per_xcd;    // resident workgroups per XCD: the grid is 8 * min(that, wg_per_xcd)
+  // Work-queue counters for the persistent form of the kernel (9 int32 on the device,
+  // zero between launches: the kernel resets them), or null for one workgroup per unit.
+  // Used at d = 64 only.
+  int* queue;
   float* ws_parts;         // parts, fp32 [slot][fwd_rows_per_workgroup(d)][d + 4]: O/l, log-sum-exp
 };
 

@@ -395,6 +395,7 @@ struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
   std::vector<void*> retired;
+  int* queue = nullptr;  // the forward kernel's work-queue counters, never replaced
 };
 std::map<std::pair<int, void*>, Workspace> g_workspaces;
 
@@ -431,6 +432,24 @@ int check_args(const void* q, const void* k, const void* v, void* out, int B, in
 }
 
 
+int queue_for(int dev, void* stream, int** out) {
+  std::lock_guard<std::mutex> lock(g_cache_mutex);
+  Workspace& ws = g_workspaces[{dev, stream}];
+  if (!ws.queue) {
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, 64 * sizeof(int));
+    if (e != hipSuccess) return fail(TA_ERR_HIP, std::string("hipMalloc: ") + hipGetErrorString(e));
+    e = hipMemset(p, 0, 64 * sizeof(int));
+    if (e != hipSuccess) {
+      (void)hipFree(p);
+      return fail(TA_ERR_HIP, std::string("hipMemset: ") + hipGetErrorString(e));
+    }
+    ws.queue = static_cast<int*>(p);
+  }
+  *out = ws.queue;
+  return TA_OK;
+}
+
 // Workspace of at least `bytes` for (dev, stream). One that is too small is replaced
 // by a larger one (at least 1.5 times the old size, so replacements stay few) and
 // kept allocated until process exit: work already enqueued with it, or being
@@ -459,7 +478,7 @@ int workspace_for(int dev, void* stream, size_t bytes, void** out) {
 
 int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, int H, int F,
                 int T, int d, int P, const DeviceWorkList& plan, float* ws, float scale,
-                float* lse, void* stream) {
+                float* lse, void* stream, int* queue, int slots_x) {
   const DeviceWorkList* wl = &plan;
   const int L = std::max(T, P);
   const int64_t nqb = (L + ta::fwd_rows_per_workgroup(d) - 1) / ta::fwd_rows_per_workgroup(d);
@@ -487,6 +506,8 @@ int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, i
   a.cut_units = wl->cut_units;
   a.n_cut_units = wl->n_cut_units;
   a.wg_per_xcd = wl->wg_per_xcd;
+  a.slots_per_xcd = std::max(1, slots_x);
+  a.queue = queue;
   a.lse = lse;
   // Logits are formed from |scale| (a negative scale flips the sign of q, which
   // is exact in bf16). scale == 0 zeroes q instead, so every logit is exactly 0
@@ -568,7 +589,15 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
     st = workspace_for(dev, stream, ws_bytes(*wl), &ws);
     if (st != TA_OK) return st;
   }
-  st = enqueue_fwd(q, k, v, out, B, H, F, T, d, P, *wl, static_cast<float*>(ws), scale, lse, stream);
+  // The MM-DiT form at d = 64 with split frames runs the kernel's persistent work loop:
+  // its units mix pieces of the text and global rows, short video units and empty text
+  // query blocks, and the hardware's in-order dispatch of one workgroup per unit left
+  // slots idle (measured at the CogVideoX shape with one global frame). Without split
+  // frames, and for the video-only form, one workgroup per unit was as fast or faster.
+  int* queue = nullptr;
+  if (P > 0 && d == 64 && wl->n_heavy > 0 && (st = queue_for(dev, stream, &queue)) != TA_OK) return st;
+  st = enqueue_fwd(q, k, v, out, B, H, F, T, d, P, *wl, static_cast<float*>(ws), scale, lse, stream, queue,
+                   fl.slots_x);
   if (st != TA_OK) return st;
   g_last_error.clear();
   return TA_OK;

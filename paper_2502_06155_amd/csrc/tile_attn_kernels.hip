@@ -297,7 +297,7 @@ struct FwdItem {
 // end of a segment with at most 32 valid rows per wave runs with QB = 1, so no wave
 // computes a column block that lies wholly past the segment end.
 template <int D, bool PREFIX, int QB, bool PARTS>
-__device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>& lay,
+__device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layout<PREFIX>& lay,
                                          uint16_t (&sK)[2][Shape<D>::kTileElems],
                                          uint16_t (&sV)[2][Shape<D>::kTileElems],
                                          float* __restrict__ ws_o, float* __restrict__ ws_lse,
@@ -318,8 +318,11 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
   const int seg0 = it.seg0, seg_len = it.seg_len;
   [[maybe_unused]] const int F = lay.F, T = lay.T, P = lay.P;
 
-  const int tid = threadIdx.x;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  // The lane id is read here (an asm statement the compiler cannot hoist), so nothing
+  // lane-dependent is held in vector registers across the caller's work loop; the
+  // wave index comes in as a scalar.
+  int lane;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
   const int n = lane & 31, hf = lane >> 5;
 
   // This lane's two query rows (within the frame), one per 32-query column block,
@@ -604,29 +607,24 @@ __device__ __forceinline__ void fwd_rows(const FwdItem& it, const Layout<PREFIX>
   }
 }
 
-// Work of one launch. Logical unit u = (batch entry b, item i, query block qb), qb
+// One unit of work. Logical unit u = (batch entry b, item i, query block qb), qb
 // fastest, covers the item's kept tiles for kBlockQ query rows. XCD x (the workgroups
-// with blockIdx % 8 == x; each XCD has its own L2) runs, in order, the units
-// [start_x, start_x + n_dp_x) one per workgroup, then n_part_x workgroups that each take
-// one part of a unit that would otherwise run in a ragged last round of whole units:
-// a piece {u, first tile, tiles, partial slot}. sched holds {start_x, n_dp_x, n_part_x,
-// first piece} per XCD, then the pieces. Launches without parts (PARTS false) take the
-// whole units of each XCD from the same contiguous shares, computed in place.
-
+// with blockIdx % 8 == x; each XCD has its own L2) owns the positions 0 .. n_x - 1 of
+// its queue: positions below n_dp_x are the units start_x + pos, run whole; the
+// n_part_x after them are parts of the units that would otherwise make a ragged last
+// round of whole units, each a piece {u, first tile, tiles, partial slot}. sched holds
+// {start_x, n_dp_x, n_part_x, first piece} per XCD, then the pieces. Launches without
+// parts (PARTS false) give XCD x the contiguous units [x q + min(x, r), + q + (x < r))
+// of the n = q 8 + r units, computed in place.
 template <int D, bool PREFIX, bool PARTS>
-__global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
-    const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
-    const uint16_t* __restrict__ V, uint16_t* __restrict__ O,
-    const int32_t* __restrict__ items, const int32_t* __restrict__ cols, int n_items, int B,
-    int H, int F, int T, int P, int nqb, const int32_t* __restrict__ sched,
-    float* __restrict__ ws_o, float* __restrict__ ws_lse, float* __restrict__ lse,
-    float* __restrict__ ws_parts, float c, uint32_t qflip, uint32_t qmask) {
-  using Sh = Shape<D>;
+__device__ __forceinline__ void fwd_unit(
+    int wave, uint32_t x, int pos, const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
+    const uint16_t* __restrict__ V, uint16_t* __restrict__ O, const int32_t* __restrict__ items,
+    const int32_t* __restrict__ cols, int n_items, int B, int H, int F, int T, int P, int nqb,
+    const int32_t* __restrict__ sched, float* __restrict__ ws_o, float* __restrict__ ws_lse,
+    float* __restrict__ lse, float* __restrict__ ws_parts, float c, uint32_t qflip, uint32_t qmask,
+    uint16_t (&sK)[2][Shape<D>::kTileElems], uint16_t (&sV)[2][Shape<D>::kTileElems]) {
   constexpr int kBlockQ = fwd_rows_per_wg<D>();
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
-
-  const uint32_t x = blockIdx.x % 8, pos = blockIdx.x / 8;
   const uint32_t per_b = (uint32_t)n_items * (uint32_t)nqb;
   FwdItem it;
   it.t0 = 0;
@@ -634,19 +632,15 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
   it.part = -1;
   uint32_t u;
   if constexpr (!PARTS) {
-    // Without parts the schedule gives XCD x the contiguous units [x q + min(x, r), + q +
-    // (x < r)) of the n = q 8 + r units, which need no table lookup.
     const uint32_t n = (uint32_t)B * per_b, q = n / 8, r = n % 8;
-    if (pos >= q + (x < r ? 1u : 0u)) return;
-    u = x * q + min(x, r) + pos;
+    u = x * q + min(x, r) + (uint32_t)pos;
   } else {
     const int32_t* xi = sched + 4 * x;
     const int n_dp = xi[1];
-    if ((int)pos < n_dp) {
-      u = (uint32_t)xi[0] + pos;
+    if (pos < n_dp) {
+      u = (uint32_t)xi[0] + (uint32_t)pos;
     } else {
-      if ((int)pos >= n_dp + xi[2]) return;
-      const int32_t* pc = sched + 32 + 4 * (xi[3] + (int)pos - n_dp);
+      const int32_t* pc = sched + 32 + 4 * (xi[3] + pos - n_dp);
       u = (uint32_t)pc[0];
       it.t0 = pc[1];
       it.nt = pc[2];
@@ -654,41 +648,133 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(
     }
   }
   const Layout<PREFIX> lay{F, T, P};
-  {
-    it.B = (uint32_t)B;
-    it.b = u / per_b;
-    const uint32_t rem = u - it.b * per_b;
-    const int32_t* item = items + 5 * (rem / nqb);
-    it.bh = it.b * (uint32_t)H + (uint32_t)item[0];
-    it.frame = item[1];
-    it.kbeg = item[2];
-    it.n_kept = item[3];
-    it.slot = item[4];  // >= 0: a piece of a split frame, written as a partial
-    it.qb = (int)(rem % nqb);
-    it.cols = cols;
-    it.seg0 = lay.start(it.frame);
-    it.seg_len = lay.len(it.frame);
-    // With a prefix the text segment is shorter than the grid's query blocks assume.
-    if (PREFIX && it.qb * kBlockQ >= it.seg_len) return;
+  it.B = (uint32_t)B;
+  it.b = u / per_b;
+  const uint32_t rem = u - it.b * per_b;
+  const int32_t* item = items + 5 * (rem / nqb);
+  it.bh = it.b * (uint32_t)H + (uint32_t)item[0];
+  it.frame = item[1];
+  it.kbeg = item[2];
+  it.n_kept = item[3];
+  it.slot = item[4];  // >= 0: a piece of a split frame, written as a partial
+  it.qb = (int)(rem % nqb);
+  it.cols = cols;
+  it.seg0 = lay.start(it.frame);
+  it.seg_len = lay.len(it.frame);
+  // With a prefix the text segment is shorter than the grid's query blocks assume.
+  if (PREFIX && it.qb * kBlockQ >= it.seg_len) return;
 
-    it.head_rows = (size_t)P * PREFIX + (size_t)F * T;
-    const size_t head_elems = it.head_rows * D;
-    it.Qh = Q + it.bh * head_elems;
-    it.Kh = K + it.bh * head_elems;
-    it.Vh = V + it.bh * head_elems;
-    it.Oh = O + it.bh * head_elems;
+  it.head_rows = (size_t)P * PREFIX + (size_t)F * T;
+  const size_t head_elems = it.head_rows * D;
+  it.Qh = Q + it.bh * head_elems;
+  it.Kh = K + it.bh * head_elems;
+  it.Vh = V + it.bh * head_elems;
+  it.Oh = O + it.bh * head_elems;
 
-    // A query block at the end of a segment with at most 32 valid rows per wave runs
-    // with one column block per wave. Only at d = 64: at d = 96 the second instance of
-    // the tile loop makes the register allocator spill the main one.
-    if constexpr (fwd_q_blocks<D>() == 2 && D == 64) {
-      if (it.seg_len - it.qb * kBlockQ <= kWaves * 32) {
-        fwd_rows<D, PREFIX, 1, PARTS>(it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip, qmask);
-        return;
-      }
+  // A query block at the end of a segment with at most 32 valid rows per wave runs
+  // with one column block per wave. Only at d = 64: at d = 96 the second instance of
+  // the tile loop makes the register allocator spill the main one.
+  if constexpr (fwd_q_blocks<D>() == 2 && D == 64) {
+    if (it.seg_len - it.qb * kBlockQ <= kWaves * 32) {
+      fwd_rows<D, PREFIX, 1, PARTS>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip, qmask);
+      return;
     }
-    fwd_rows<D, PREFIX, fwd_q_blocks<D>(), PARTS>(it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip,
-                                                  qmask);
+  }
+  fwd_rows<D, PREFIX, fwd_q_blocks<D>(), PARTS>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip,
+                                                qmask);
+}
+
+// The forward kernel's arguments, passed by value (they live in the kernel-argument
+// segment, where the work loop reads them again for every unit).
+struct FwdKernelArgs {
+  const uint16_t* Q;
+  const uint16_t* K;
+  const uint16_t* V;
+  uint16_t* O;
+  const int32_t* items;
+  const int32_t* cols;
+  const int32_t* sched;
+  float* ws_o;
+  float* ws_lse;
+  float* lse;
+  float* ws_parts;
+  int* queue;
+  int n_wg;  // the grid size
+  int n_items, B, H, F, T, P, nqb;
+  float c;
+  uint32_t qflip, qmask;
+};
+
+// The kernel. Without PERSIST, one workgroup per queue position: workgroup blockIdx
+// takes position blockIdx / 8 of XCD blockIdx % 8 (the hardware hands workgroup ids to
+// the eight XCDs in turn), and the in-order dispatcher starts each as a slot frees.
+// With PERSIST, a work loop: at most the resident number of workgroups per XCD, each
+// taking the next position of its XCD's queue (queue[x], an atomic counter) until the
+// queue is exhausted. For the plans the host selects (the MM-DiT form with split
+// frames: pieces of the text and global rows, short video units and empty text query
+// blocks), the dispatcher leaves slots idle that the loop keeps busy. The queue
+// counters start at zero; the last workgroup to finish (counted in queue[8]) sets all
+// nine back to zero for the next launch on the same queue. No workgroup ever waits
+// for another.
+template <int D, bool PREFIX, bool PARTS, bool PERSIST>
+__global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(const FwdKernelArgs args) {
+  using Sh = Shape<D>;
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
+
+  const uint32_t x = blockIdx.x % 8;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // Queue positions of XCD y.
+  auto positions = [](uint32_t y, int B, int n_items, int nqb, const int32_t* sched) {
+    if constexpr (!PARTS) {
+      const uint32_t n = (uint32_t)B * (uint32_t)n_items * (uint32_t)nqb;
+      return (int)(n / 8 + (y < n % 8 ? 1u : 0u));
+    } else {
+      return sched[4 * y + 1] + sched[4 * y + 2];
+    }
+  };
+  if constexpr (!PERSIST) {
+    const int pos = (int)(blockIdx.x / 8);
+    if (pos >= positions(x, args.B, args.n_items, args.nqb, args.sched)) return;
+    fwd_unit<D, PREFIX, PARTS>(wave, x, pos, args.Q, args.K, args.V, args.O, args.items, args.cols,
+                               args.n_items, args.B, args.H, args.F, args.T, PREFIX ? args.P : 0, args.nqb,
+                               args.sched, args.ws_o, args.ws_lse, args.lse, args.ws_parts, args.c, args.qflip,
+                               args.qmask, sK, sV);
+  } else {
+    __shared__ int s_pos[2];
+    // The arguments are read from the argument segment where they are needed, through a
+    // pointer the compiler cannot see is loop-invariant, so that no argument is held in
+    // a scalar register across the loop (the tile loop needs them all); the lane id is
+    // read the same way.
+    using KArgPtr = const __attribute__((address_space(4))) FwdKernelArgs*;
+    auto fresh_args = []() {
+      KArgPtr ap = (KArgPtr)__builtin_amdgcn_kernarg_segment_ptr();
+      asm volatile("" : "+s"(ap));
+      return ap;
+    };
+    auto first_thread = [&]() {
+      int lane;
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+      return wave == 0 && lane == 0;
+    };
+    // s_pos alternates between two words, so thread 0 never overwrites a position
+    // another wave has yet to read (one barrier between each write and its reads).
+    for (int round = 0;; ++round) {
+      KArgPtr ap = fresh_args();
+      if (first_thread()) s_pos[round & 1] = atomicAdd(ap->queue + x, 1);
+      __syncthreads();
+      const int pos = __builtin_amdgcn_readfirstlane(s_pos[round & 1]);
+      if (pos >= positions(x, ap->B, ap->n_items, ap->nqb, ap->sched)) break;
+      fwd_unit<D, PREFIX, PARTS>(wave, x, pos, ap->Q, ap->K, ap->V, ap->O, ap->items, ap->cols,
+                                 ap->n_items, ap->B, ap->H, ap->F, ap->T, PREFIX ? ap->P : 0, ap->nqb,
+                                 ap->sched, ap->ws_o, ap->ws_lse, ap->lse, ap->ws_parts, ap->c, ap->qflip,
+                                 ap->qmask, sK, sV);
+    }
+    KArgPtr ap = fresh_args();
+    if (first_thread() && atomicAdd(ap->queue + 8, 1) == ap->n_wg - 1) {
+#pragma unroll
+      for (int i = 0; i < 9; ++i) atomicExch(ap->queue + i, 0);
+    }
   }
 }
 
@@ -802,13 +888,22 @@ __global__ __launch_bounds__(256) void merge_partials_kernel(
 template <int D>
 hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
   const int nqb = (std::max(a.T, a.P) + fwd_rows_per_wg<D>() - 1) / fwd_rows_per_wg<D>();
-  const dim3 grid(8u * (uint32_t)a.wg_per_xcd);
-  // The kernel that can run parts of units only where the schedule has some.
+  // The work loop where the host asks for it (and only at d = 64: at d = 96 it would
+  // cost the tile loop registers it does not have); the kernel that can run parts of
+  // units only where the schedule has some.
+  const bool persist = a.queue != nullptr && a.P > 0 && D == 64;
+  const dim3 grid(8u * (uint32_t)(persist ? std::min(a.wg_per_xcd, a.slots_per_xcd) : a.wg_per_xcd));
   auto go = [&](auto prefix, auto parts) {
     constexpr bool kPrefix = decltype(prefix)::value, kParts = decltype(parts)::value;
-    hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kParts>), grid, dim3(kThreads), 0, stream, a.q,
-                       a.k, a.v, a.out, a.items, a.cols, a.n_items, a.B, a.H, a.F, a.T, kPrefix ? a.P : 0,
-                       nqb, a.sched, a.ws_o, a.ws_lse, a.lse, a.ws_parts, a.c, a.qflip, a.qmask);
+    const FwdKernelArgs ka{a.q,      a.k,   a.v,        a.out,   a.items,         a.cols,
+                           a.sched,  a.ws_o, a.ws_lse,  a.lse,   a.ws_parts,      a.queue,
+                           (int)grid.x, a.n_items, a.B, a.H,    a.F,             a.T,
+                           kPrefix ? a.P : 0, nqb, a.c, a.qflip, a.qmask};
+    if (kPrefix && D == 64 && persist)
+      hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kParts, kPrefix && D == 64>), grid, dim3(kThreads), 0,
+                         stream, ka);
+    else
+      hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kParts, false>), grid, dim3(kThreads), 0, stream, ka);
   };
   using Y = std::true_type;
   using N = std::false_type;

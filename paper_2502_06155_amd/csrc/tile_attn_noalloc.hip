@@ -112,7 +112,8 @@ extern "C" int tile_attn_fwd_heads_noalloc(const void* q, const void* k, const v
   }
   const DeviceWorkList wl = place_work_list(hw, base);
   float* partials = reinterpret_cast<float*>(base + kPlanWords);
-  st = enqueue_fwd(q, k, v, out, B, H, F, T, d, 0, wl, partials, scale, lse, stream);
+  // No text prefix here, so one workgroup per unit (no work-queue counters).
+  st = enqueue_fwd(q, k, v, out, B, H, F, T, d, 0, wl, partials, scale, lse, stream, nullptr, slots_x);
   if (st != TA_OK) return st;
   clear_error();
   return TA_OK;

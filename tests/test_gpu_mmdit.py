@@ -157,3 +157,53 @@ def test_mmdit_ragged_round_in_parts():
     for hh in (0, H - 1):
         ref_lse = ommd.attention_mmdit_lse(qb[:, hh:hh + 1], kb[:, hh:hh + 1], mask, T, P, scale)
         assert_lse(lse[:, hh:hh + 1], ref_lse, f"mmdit-parts-lse-h{hh}")
+
+
+def test_mmdit_work_queue_in_graph_and_between_calls():
+    """The MM-DiT form at d = 64 with split frames runs the kernel's persistent work
+    loop, whose queue counters (per stream) every launch must leave at zero: eager
+    calls of two shapes in turn on one stream, then a captured graph replayed several
+    times with eager calls in between, all equal their first eager result bit for bit."""
+    d, P = 64, 77
+    shapes = [(1, 6, 11, 300), (2, 3, 12, 130)]
+    inputs = []
+    for i, (B, H, F, T) in enumerate(shapes):
+        qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=900 + i, prefix=P)
+        mask = om.tile_mask(F, 1, "sym")
+        aug = np.ones((F + 1, F + 1), np.uint8)  # the text segment's row and column kept
+        aug[:F, :F] = mask
+        assert ta.tile_attn_plan(aug)[1] > 0  # split frames: the persistent loop runs
+        inputs.append((qb, kb, vb, mask, T))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    dev = []
+    with torch.cuda.stream(s):
+        for qb, kb, vb, masks, T in inputs:
+            q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+            dev.append((q, k, v, torch.empty_like(q), masks, T))
+
+    def call(i):
+        q, k, v, out, masks, T = dev[i]
+        B, H, S, _ = q.shape
+        ta.tile_attn_fwd_mmdit(q, k, v, out, B, H, (S - P) // T, T, P, d, masks, d ** -0.5, None, s)
+
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            call(0)
+            call(1)
+    s.synchronize()
+    first = [from_dev(x[3]) for x in dev]
+    for i, (qb, kb, vb, masks, T) in enumerate(inputs):
+        assert_parity(first[i], ommd.attention_mmdit(qb, kb, vb, masks, T, P, d ** -0.5), f"queue-{i}")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        call(0)
+    for rep in range(3):
+        dev[0][3].fill_(float("nan"))
+        with torch.cuda.stream(s):
+            call(1)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(from_dev(dev[0][3]), first[0]), rep
+        assert np.array_equal(from_dev(dev[1][3]), first[1]), rep
