@@ -519,8 +519,8 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
     __syncthreads();
 
     // dP - delta of 32-query half qc of the tile: the accumulation starts at the rows' -delta
-    // (entry 8 c2 + 4u + j holds query row 32 qc + 16 c2 + 8u + 4h + j), read before
-    // both halves' S so that the reads land while S forms.
+    // (entry 8 c2 + 4u + j holds query row 32 qc + 16 c2 + 8u + 4h + j), read at the
+    // half's first packet.
     auto dp_start = [&](int buf, int qc, f32x16& dp) {
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2)
@@ -531,191 +531,136 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
           for (int j = 0; j < 4; ++j) dp[8 * c2 + 4 * u + j] = d4[j];
         }
     };
-    // S of half qc.
-    auto s_chain = [&](int buf, int qc, f32x16& sc) {
-      sc = f32x16{};
-#pragma unroll
-      for (int cc = 0; cc < Sh::kChunks; ++cc) sc = mfma32(row_frag<D>(sQ[buf], ra, qc, cc), kf[cc], sc);
-    };
-    auto dp_chain = [&](int buf, int qc, f32x16& dp) {
-#pragma unroll
-      for (int cc = 0; cc < Sh::kChunks; ++cc) dp = mfma32(row_frag<D>(sG[buf], ra, qc, cc), vf[cc], dp);
-    };
-    // P and dS of half qc as B operands (entry 8 c2 + 4u + j holds query row
-    // 32 qc + 16 c2 + 8u + 4h + j).
-    auto grads = [&](int buf, int qc, const f32x16& sc, const f32x16& dp, bf16x8 (&pb)[2],
-                     bf16x8 (&db)[2]) {
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2) {
-        f32x8 p8, d8;
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sL[buf][32 * qc + 16 * c2 + 8 * u + 4 * hf]);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int e = 8 * c2 + 4 * u + j;
-            const float p = prob(sc[e], a.c, l4[j]);
-            p8[4 * u + j] = p;
-            d8[4 * u + j] = p * dp[e];  // dp holds dP - delta
-          }
-        }
-        if constexpr (kWantDv) pb[c2] = __builtin_convertvector(p8, bf16x8);
-        if constexpr (kWantDk) db[c2] = __builtin_convertvector(d8, bf16x8);
-      }
-    };
-    // dV^T += dO^T P and dK^T += Q^T dS over half qc.
-    auto accumulate = [&](int buf, int qc, const bf16x8 (&pb)[2], const bf16x8 (&db)[2]) {
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-        for (int mb = 0; mb < Sh::kDBlocks; ++mb) {
-          if constexpr (kWantDv) dv[mb] = mfma32(tr_frag<D>(sG[buf], ta, mb, 2 * qc + c2), pb[c2], dv[mb]);
-          if constexpr (kWantDk) dk[mb] = mfma32(tr_frag<D>(sQ[buf], ta, mb, 2 * qc + c2), db[c2], dk[mb]);
-        }
-    };
-
     // One tile; the buffer index is a compile-time constant (the loop below runs tiles
     // in pairs), so every LDS address is a per-lane base plus an immediate offset.
     auto tile_step = [&](auto bufc, int t) {
       constexpr int buf = decltype(bufc)::value;
       if (t + 1 < n_tiles) load_tile(nxt, buf ^ 1);
       if (wave_active) {
-        if constexpr (MODE != kDkOnly) {
-          // One stream of MFMAs (8 D/16 per tile for dV and dK together), each in a
-          // fenced packet with its share of the vector work; the operand fragment of
-          // MFMA i is read from LDS at packet i - 2 into one of three rotating
-          // registers, so no MFMA waits on a read issued just before it (3.5% faster
-          // than leaving the order to the compiler). Stream: S (and dP) of half 0, S
-          // (and dP) of half 1 with half 0's P (and dS) forming, the dV/dK update of
-          // half 0 with half 1's P (and dS) forming, the update of half 1. The dV pass
-          // of d = 128 (S, P, dV) runs the same stream without dP, dS and dK; the dK
-          // pass (S, dP, dS, dK) would need three registers more than it has.
-          constexpr int kC = Sh::kChunks, kMb = Sh::kDBlocks;
-          constexpr int kHalf = (kWantDk ? 2 : 1) * kC;                   // S (+ dP) MFMAs of a half
-          constexpr int kAcc = ((int)kWantDv + (int)kWantDk) * 2 * kMb;  // update MFMAs of a half
-          constexpr int kN = 2 * kHalf + 2 * kAcc;                        // the whole stream
-          constexpr int kPerC2 = kAcc / 2;                                 // update MFMAs per chunk
-          f32x16 sc[2], dp[kWantDk ? 2 : 1];
-          bf16x8 pb[kWantDv ? 2 : 1][2], db[kWantDk ? 2 : 1][2];
-          f32x4 l4[2][4];  // lse2 of this lane's 16 queries of each half, 4 at a time
-          // Update MFMA r of a half: chunk c2, d-block mb, dK (else dV).
-          auto upd = [](int r, int& c2, int& mb, bool& is_dk) {
-            c2 = r / kPerC2;
-            const int q = r % kPerC2;
-            if (kWantDv && kWantDk) {
-              mb = q / 2;
-              is_dk = q % 2;
+        // One stream of MFMAs (8 D/16 per tile for dV and dK together), each in a
+        // fenced packet with its share of the vector work; the operand fragment of
+        // MFMA i is read from LDS at packet i - 2 into one of three rotating
+        // registers (i - 1 and two registers in the dK pass of d = 128), so no MFMA
+        // waits on a read issued just before it (3.5% faster than leaving the order to
+        // the compiler). Stream: S (and dP) of half 0, S
+        // (and dP) of half 1 with half 0's P (and dS) forming, the dV/dK update of
+        // half 0 with half 1's P (and dS) forming, the update of half 1. The passes of
+        // d = 128 run the same stream: the dV pass (S, P, dV) without dP, dS and dK,
+        // the dK pass (S, dP, dS, dK) without P and dV and with each fragment read one
+        // packet ahead into two registers (two ahead would need more registers than it
+        // has; the stream is 4.5% faster than the compiler's order there).
+        constexpr int kC = Sh::kChunks, kMb = Sh::kDBlocks;
+        constexpr int kAhead = MODE == kDkOnly ? 1 : 2;  // packets between a read and its use
+        constexpr int kHalf = (kWantDk ? 2 : 1) * kC;                   // S (+ dP) MFMAs of a half
+        constexpr int kAcc = ((int)kWantDv + (int)kWantDk) * 2 * kMb;  // update MFMAs of a half
+        constexpr int kN = 2 * kHalf + 2 * kAcc;                        // the whole stream
+        constexpr int kPerC2 = kAcc / 2;                                 // update MFMAs per chunk
+        f32x16 sc[2], dp[kWantDk ? 2 : 1];
+        bf16x8 pb[kWantDv ? 2 : 1][2], db[kWantDk ? 2 : 1][2];
+        f32x4 l4[2][4];  // lse2 of this lane's 16 queries of each half, 4 at a time
+        // Update MFMA r of a half: chunk c2, d-block mb, dK (else dV).
+        auto upd = [](int r, int& c2, int& mb, bool& is_dk) {
+          c2 = r / kPerC2;
+          const int q = r % kPerC2;
+          if (kWantDv && kWantDk) {
+            mb = q / 2;
+            is_dk = q % 2;
+          } else {
+            mb = q;
+            is_dk = kWantDk;
+          }
+        };
+        auto frag = [&](auto ic) -> bf16x8 {
+          constexpr int i = decltype(ic)::value;
+          if constexpr (i < 2 * kHalf) {
+            constexpr int h = i / kHalf, r = i % kHalf;
+            if constexpr (r < kC) return row_frag<D>(sQ[buf], ra, h, r);
+            else return row_frag<D>(sG[buf], ra, h, r - kC);
+          } else {
+            constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
+            int c2, mb;
+            bool is_dk;
+            upd(r, c2, mb, is_dk);
+            return tr_frag<D>(is_dk ? sQ[buf] : sG[buf], ta, mb, 2 * h + c2);
+          }
+        };
+        auto mfma = [&](auto ic, const bf16x8& f) {
+          constexpr int i = decltype(ic)::value;
+          if constexpr (i < 2 * kHalf) {
+            constexpr int h = i / kHalf, r = i % kHalf;
+            if constexpr (r < kC) sc[h] = mfma32(f, kf[r], r == 0 ? f32x16{} : sc[h]);
+            else if constexpr (kWantDk) dp[h] = mfma32(f, vf[r - kC], dp[h]);
+          } else {
+            constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
+            int c2, mb;
+            bool is_dk;
+            upd(r, c2, mb, is_dk);
+            if constexpr (kWantDk && kWantDv) {
+              if (is_dk) dk[mb] = mfma32(f, db[h][c2], dk[mb]);
+              else dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
+            } else if constexpr (kWantDk) {
+              dk[mb] = mfma32(f, db[h][c2], dk[mb]);
             } else {
-              mb = q;
-              is_dk = kWantDk;
+              dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
             }
-          };
-          auto frag = [&](auto ic) -> bf16x8 {
-            constexpr int i = decltype(ic)::value;
-            if constexpr (i < 2 * kHalf) {
-              constexpr int h = i / kHalf, r = i % kHalf;
-              if constexpr (r < kC) return row_frag<D>(sQ[buf], ra, h, r);
-              else return row_frag<D>(sG[buf], ra, h, r - kC);
-            } else {
-              constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
-              int c2, mb;
-              bool is_dk;
-              upd(r, c2, mb, is_dk);
-              return tr_frag<D>(is_dk ? sQ[buf] : sG[buf], ta, mb, 2 * h + c2);
-            }
-          };
-          auto mfma = [&](auto ic, const bf16x8& f) {
-            constexpr int i = decltype(ic)::value;
-            if constexpr (i < 2 * kHalf) {
-              constexpr int h = i / kHalf, r = i % kHalf;
-              if constexpr (r < kC) sc[h] = mfma32(f, kf[r], r == 0 ? f32x16{} : sc[h]);
-              else if constexpr (kWantDk) dp[h] = mfma32(f, vf[r - kC], dp[h]);
-            } else {
-              constexpr int j = i - 2 * kHalf, h = j / kAcc, r = j % kAcc;
-              int c2, mb;
-              bool is_dk;
-              upd(r, c2, mb, is_dk);
-              if constexpr (kWantDk && kWantDv) {
-                if (is_dk) dk[mb] = mfma32(f, db[h][c2], dk[mb]);
-                else dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
-              } else if constexpr (kWantDk) {
-                dk[mb] = mfma32(f, db[h][c2], dk[mb]);
-              } else {
-                dv[mb] = mfma32(f, pb[h][c2], dv[mb]);
-              }
-            }
-          };
-          // Vector work of packet i: LDS reads of -delta (dP starts) and lse2 ahead of
-          // their use, and P (and dS) of half 0 over the second half's S/dP packets, of
-          // half 1 over half 0's update packets, 2 queries at a time.
-          auto side = [&](auto ic) {
-            constexpr int i = decltype(ic)::value;
-            if constexpr (kWantDk && (i == 0 || i == kHalf)) dp_start(buf, i / kHalf, dp[i / kHalf]);
-            // lse2 of queries 4 q4 .. 4 q4 + 3 (entries 4 q4 ..) of half hh, read two
-            // packets before the first packet whose share needs them.
-            static_for<8>([&](auto qc) {
-              constexpr int hh = decltype(qc)::value / 4, q4 = decltype(qc)::value % 4;
-              constexpr int st = hh == 0 ? kHalf : 2 * kHalf, pk = hh == 0 ? kHalf : kAcc;
-              constexpr int at = st + ((2 * q4 + 1) * pk + 7) / 8 - 1 - 2;
-              if constexpr (at == i)
-                l4[hh][q4] = *reinterpret_cast<const f32x4*>(&sL[buf][32 * hh + 16 * (q4 / 2) + 8 * (q4 % 2) + 4 * hf]);
-            });
-            constexpr int h = i < kHalf ? -1 : (i < 2 * kHalf ? 0 : (i < 2 * kHalf + kAcc ? 1 : -1));
-            if constexpr (h >= 0) {
-              constexpr int k = h == 0 ? i - kHalf : i - 2 * kHalf;  // packet within the share
-              constexpr int kPk = h == 0 ? kHalf : kAcc;
-#pragma unroll
-              for (int u = k * 8 / kPk; u < (k + 1) * 8 / kPk; ++u) {
-                // queries e, e+1 of the half: entry e = 8 c2 + 4 uu + j
-                const int e = 2 * u, c2 = e / 8, uu = (e % 8) / 4, j = e % 4;
-                const float p0 = prob(sc[h][e], a.c, l4[h][2 * c2 + uu][j]);
-                const float p1 = prob(sc[h][e + 1], a.c, l4[h][2 * c2 + uu][j + 1]);
-                if constexpr (kWantDv) {
-                  const f32x2 pp = {p0, p1};
-                  const bf16x2 pq = __builtin_convertvector(pp, bf16x2);
-                  u32x4 pw = __builtin_bit_cast(u32x4, pb[h][c2]);
-                  pw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, pq);
-                  pb[h][c2] = __builtin_bit_cast(bf16x8, pw);
-                }
-                if constexpr (kWantDk) {
-                  const f32x2 dd = {p0 * dp[h][e], p1 * dp[h][e + 1]};
-                  const bf16x2 dq = __builtin_convertvector(dd, bf16x2);
-                  u32x4 dw = __builtin_bit_cast(u32x4, db[h][c2]);
-                  dw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, dq);
-                  db[h][c2] = __builtin_bit_cast(bf16x8, dw);
-                }
-              }
-            }
-          };
-          bf16x8 fr[3];
-          fr[0] = frag(std::integral_constant<int, 0>{});
-          fr[1] = frag(std::integral_constant<int, 1>{});
-          __builtin_amdgcn_sched_barrier(0);
-          static_for<kN>([&](auto ic) {
-            constexpr int i = decltype(ic)::value;
-            if constexpr (i + 2 < kN) fr[(i + 2) % 3] = frag(std::integral_constant<int, i + 2>{});
-            mfma(ic, fr[i % 3]);
-            side(ic);
-            __builtin_amdgcn_sched_barrier(0);
+          }
+        };
+        // Vector work of packet i: LDS reads of -delta (dP starts) and lse2 ahead of
+        // their use, and P (and dS) of half 0 over the second half's S/dP packets, of
+        // half 1 over half 0's update packets, 2 queries at a time.
+        auto side = [&](auto ic) {
+          constexpr int i = decltype(ic)::value;
+          if constexpr (kWantDk && (i == 0 || i == kHalf)) dp_start(buf, i / kHalf, dp[i / kHalf]);
+          // lse2 of queries 4 q4 .. 4 q4 + 3 (entries 4 q4 ..) of half hh, read two
+          // packets before the first packet whose share needs them.
+          static_for<8>([&](auto qc) {
+            constexpr int hh = decltype(qc)::value / 4, q4 = decltype(qc)::value % 4;
+            constexpr int st = hh == 0 ? kHalf : 2 * kHalf, pk = hh == 0 ? kHalf : kAcc;
+            constexpr int at = st + ((2 * q4 + 1) * pk + 7) / 8 - 1 - kAhead;
+            if constexpr (at == i)
+              l4[hh][q4] = *reinterpret_cast<const f32x4*>(&sL[buf][32 * hh + 16 * (q4 / 2) + 8 * (q4 % 2) + 4 * hf]);
           });
-        } else {
-          // The dK pass at d = 128: both halves' -delta reads, S, then dP (so the reads
-          // land while S forms), then half 0's P and dS and update ahead of half 1's;
-          // the compiler interleaves them (fencing the phases, as in the dq pass,
-          // measured 4% slower here).
-          f32x16 s0, dp0, s1, dp1;
-          bf16x8 pb0[2], db0[2], pb1[2], db1[2];
-          dp_start(buf, 0, dp0);
-          dp_start(buf, 1, dp1);
-          s_chain(buf, 0, s0);
-          s_chain(buf, 1, s1);
-          dp_chain(buf, 0, dp0);
-          dp_chain(buf, 1, dp1);
-          grads(buf, 0, s0, dp0, pb0, db0);
-          accumulate(buf, 0, pb0, db0);
-          grads(buf, 1, s1, dp1, pb1, db1);
-          accumulate(buf, 1, pb1, db1);
-        }
+          constexpr int h = i < kHalf ? -1 : (i < 2 * kHalf ? 0 : (i < 2 * kHalf + kAcc ? 1 : -1));
+          if constexpr (h >= 0) {
+            constexpr int k = h == 0 ? i - kHalf : i - 2 * kHalf;  // packet within the share
+            constexpr int kPk = h == 0 ? kHalf : kAcc;
+#pragma unroll
+            for (int u = k * 8 / kPk; u < (k + 1) * 8 / kPk; ++u) {
+              // queries e, e+1 of the half: entry e = 8 c2 + 4 uu + j
+              const int e = 2 * u, c2 = e / 8, uu = (e % 8) / 4, j = e % 4;
+              const float p0 = prob(sc[h][e], a.c, l4[h][2 * c2 + uu][j]);
+              const float p1 = prob(sc[h][e + 1], a.c, l4[h][2 * c2 + uu][j + 1]);
+              if constexpr (kWantDv) {
+                const f32x2 pp = {p0, p1};
+                const bf16x2 pq = __builtin_convertvector(pp, bf16x2);
+                u32x4 pw = __builtin_bit_cast(u32x4, pb[h][c2]);
+                pw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, pq);
+                pb[h][c2] = __builtin_bit_cast(bf16x8, pw);
+              }
+              if constexpr (kWantDk) {
+                const f32x2 dd = {p0 * dp[h][e], p1 * dp[h][e + 1]};
+                const bf16x2 dq = __builtin_convertvector(dd, bf16x2);
+                u32x4 dw = __builtin_bit_cast(u32x4, db[h][c2]);
+                dw[(e % 8) / 2] = __builtin_bit_cast(uint32_t, dq);
+                db[h][c2] = __builtin_bit_cast(bf16x8, dw);
+              }
+            }
+          }
+        };
+        bf16x8 fr[kAhead + 1];
+        static_for<kAhead>([&](auto jc) {
+          constexpr int j = decltype(jc)::value;
+          fr[j] = frag(std::integral_constant<int, j>{});
+        });
+        __builtin_amdgcn_sched_barrier(0);
+        static_for<kN>([&](auto ic) {
+          constexpr int i = decltype(ic)::value;
+          if constexpr (i + kAhead < kN)
+            fr[(i + kAhead) % (kAhead + 1)] = frag(std::integral_constant<int, i + kAhead>{});
+          mfma(ic, fr[i % (kAhead + 1)]);
+          side(ic);
+          __builtin_amdgcn_sched_barrier(0);
+        });
       }
       cur = nxt;
       nxt.advance(n_keep);
