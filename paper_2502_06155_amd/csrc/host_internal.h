@@ -35,6 +35,7 @@ struct DeviceWorkList {
   const int32_t* sched_xcd = nullptr;
   const int32_t* cut_units = nullptr;
   int n_cut_units = 0, n_part_slots = 0, wg_per_xcd = 0;
+  bool unit_table = false;  // every position is a table entry (no contiguous whole units)
 };
 
 // The same plan as host words, before upload: offsets of the parts in words.
@@ -44,6 +45,7 @@ struct HostWorkList {
   int n_items = 0, n_heavy = 0, n_slots = 0;
   size_t off_xcd = 0, off_pieces = 0, off_cut_units = 0;
   int n_cut_units = 0, n_part_slots = 0, wg_per_xcd = 0;
+  bool unit_table = false;
 };
 
 // Workgroups a forward launch keeps resident per XCD (two per compute unit).
@@ -55,9 +57,11 @@ int resident_slots_per_xcd(int dev);
 // With share_tail, each XCD whose run would end in a ragged round of whole units (of
 // slots_x resident workgroups) runs that round's units in parts over the kept tiles
 // instead, one workgroup per part, merged by log-sum-exp; otherwise every unit is one
-// workgroup.
+// workgroup. With by_length, a plan that splits no frame and whose units with rows are
+// not already longest first in every XCD's share runs each share longest first (table
+// entries for every unit; query blocks past their segment's end are left out).
 void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int T, int P, int F,
-                         int slots_x, bool share_tail);
+                         int slots_x, bool share_tail, bool by_length = false);
 
 // Plans H heads with n_masks masks (1: shared, H: one per head) of F segments; heavy
 // query frames are split into pieces when allow_split.

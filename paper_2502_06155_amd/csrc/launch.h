@@ -42,6 +42,7 @@ struct FwdArgs {
   const int32_t* cut_units;
   int n_cut_units;
   int wg_per_xcd;       // queue positions of the busiest XCD
+  bool unit_table;      // every position is a piece of the table (none contiguous)
   int slots_per_xcd;    // resident workgroups per XCD: the grid is 8 * min(that, wg_per_xcd)
   // Work-queue counters for the persistent form of the kernel (9 int32 on the device,
   // zero between launches: the kernel resets them), or null for one workgroup per unit.

@@ -156,12 +156,13 @@ DeviceWorkList place_work_list(const HostWorkList& hw, void* buf) {
     wl.n_cut_units = hw.n_cut_units;
     wl.n_part_slots = hw.n_part_slots;
     wl.wg_per_xcd = hw.wg_per_xcd;
+    wl.unit_table = hw.unit_table;
   }
   return wl;
 }
 
 void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int T, int P, int F,
-                         int slots_x, bool share_tail) {
+                         int slots_x, bool share_tail, bool by_length) {
   const int32_t* items = hw.words.data();
   const int32_t* cols = hw.words.data() + hw.off_cols;
   const int64_t n_items = hw.n_items;
@@ -178,14 +179,44 @@ void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int 
   };
   const int64_t per_b = n_items * nqb, n = (int64_t)B * per_b;
   auto unit_tiles = [&](int64_t u) { return tiles_of((u % per_b) / nqb, (int)(u % nqb)); };
+  // A query block past its segment's end (the text segment is shorter than the blocks
+  // the video needs) has no rows: nothing to run.
+  auto has_rows = [&](int64_t u) {
+    const int32_t* it = items + 5 * ((u % per_b) / nqb);
+    const int seg_len = (P > 0 && it[1] == F) ? P : T;
+    return (int64_t)(u % nqb) * rows < seg_len;
+  };
   std::vector<int32_t> xcd(4 * 8), pieces, cut_units;
   int n_part_slots = 0;
   int64_t wg_max = 0;
+  // Longest first where it changes something: a plan with split frames runs the
+  // kernel's persistent loop instead (its queue takes the natural order), and a share
+  // whose units with rows already come longest first keeps the contiguous form.
   const int64_t q = n / 8, r = n % 8;
+  bool table = false;
+  if (by_length && hw.n_heavy == 0) {
+    for (int x = 0; x < 8 && !table; ++x) {
+      const int64_t start = x * q + std::min<int64_t>(x, r), cnt = q + (x < r);
+      int64_t prev = -1;
+      for (int64_t u = start; u < start + cnt && !table; ++u) {
+        if (!has_rows(u)) continue;
+        const int64_t len = unit_tiles(u);
+        table = prev >= 0 && len > prev;
+        prev = len;
+      }
+    }
+  }
+  std::vector<int64_t> us;
   for (int x = 0; x < 8; ++x) {
     const int64_t start = x * q + std::min<int64_t>(x, r), cnt = q + (x < r);
     int64_t n_dp = cnt;
     const int64_t first_piece = (int64_t)pieces.size() / 4;
+    // This XCD's units in the order it runs them: as numbered, or longest first.
+    us.resize(cnt);
+    for (int64_t i = 0; i < cnt; ++i) us[i] = start + i;
+    if (table)
+      std::stable_sort(us.begin(), us.end(),
+                       [&](int64_t a, int64_t b) { return unit_tiles(a) > unit_tiles(b); });
     // An XCD runs its whole units in rounds of slots_x. If the last round is ragged,
     // its R units can be cut into k parts each: the parts then take ceil(R k / slots_x)
     // rounds of 1/k of a unit instead of one round of whole units, and every part
@@ -196,9 +227,10 @@ void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int 
     // with split frames is left whole: its pieces, dispatched longest first, already
     // even out the last round, and parts of pieces would add a second merge.
     const int64_t ragged = cnt % slots_x;
+    int parts_k = 1;
     if (share_tail && hw.n_heavy == 0 && cnt > slots_x && ragged > 0) {
       double mean_tiles = 0;
-      for (int64_t u = start + cnt - ragged; u < start + cnt; ++u) mean_tiles += (double)unit_tiles(u);
+      for (int64_t i = cnt - ragged; i < cnt; ++i) mean_tiles += (double)unit_tiles(us[i]);
       mean_tiles /= (double)ragged;
       const double tile_s = 2.8e-6 * (rows / 256.0) * (d / 96.0);
       const double part_s = 8.0 * rows * (d + 4) * 4.0 * 2.0 / 4.0e12;  // per part, all XCDs
@@ -214,21 +246,28 @@ void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int 
       }
       if (best_k > 1 && best > 10e-6) {
         n_dp = cnt - ragged;
-        for (int64_t u = start + n_dp; u < start + cnt; ++u) {
-          const int64_t len = unit_tiles(u);
-          const int parts = (int)std::min<int64_t>(best_k, len);
-          if (parts <= 1) {  // a unit of one tile (or none) runs whole
-            if (len > 0) pieces.insert(pieces.end(), {(int32_t)u, 0, (int32_t)len, -1});
-            continue;
-          }
-          cut_units.insert(cut_units.end(), {(int32_t)u, n_part_slots, parts});
-          for (int p = 0; p < parts; ++p) {
-            const int64_t t0 = len * p / parts, t1 = len * (p + 1) / parts;
-            pieces.insert(pieces.end(), {(int32_t)u, (int32_t)t0, (int32_t)(t1 - t0), n_part_slots++});
-          }
-        }
+        parts_k = best_k;
       }
     }
+    if (table) {  // the whole units as table entries, ahead of any parts
+      for (int64_t i = 0; i < n_dp; ++i)
+        if (has_rows(us[i])) pieces.insert(pieces.end(), {(int32_t)us[i], 0, (int32_t)unit_tiles(us[i]), -1});
+    }
+    for (int64_t i = n_dp; i < cnt; ++i) {  // the ragged round, in parts
+      const int64_t u = us[i];
+      const int64_t len = unit_tiles(u);
+      const int parts = (int)std::min<int64_t>(parts_k, len);
+      if (parts <= 1) {  // a unit of one tile, or of none (its rows still get written), runs whole
+        if (has_rows(u)) pieces.insert(pieces.end(), {(int32_t)u, 0, (int32_t)len, -1});
+        continue;
+      }
+      cut_units.insert(cut_units.end(), {(int32_t)u, n_part_slots, parts});
+      for (int p = 0; p < parts; ++p) {
+        const int64_t t0 = len * p / parts, t1 = len * (p + 1) / parts;
+        pieces.insert(pieces.end(), {(int32_t)u, (int32_t)t0, (int32_t)(t1 - t0), n_part_slots++});
+      }
+    }
+    if (table) n_dp = 0;  // every position is a table entry
     const int64_t n_part = (int64_t)pieces.size() / 4 - first_piece;
     xcd[4 * x] = (int32_t)start;
     xcd[4 * x + 1] = (int32_t)n_dp;
@@ -247,6 +286,7 @@ void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int 
   hw.words.insert(hw.words.end(), cut_units.begin(), cut_units.end());
   hw.n_part_slots = n_part_slots;
   hw.wg_per_xcd = (int)wg_max;
+  hw.unit_table = table;
 }
 
 // A cached plan: its device buffer and, per stream that enqueued work with it, an
@@ -292,7 +332,7 @@ struct PlanUse {
 // The forward launch a plan is scheduled for (append_fwd_schedule).
 struct FwdLaunch {
   int B, nqb, rows, d, T, P, F, slots_x;
-  bool share_tail;
+  bool share_tail, by_length;
 };
 
 int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_split, int dev,
@@ -302,7 +342,8 @@ int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_sp
   key += std::to_string(H) + "|" + std::to_string(n_masks) + "|" + std::to_string(F) + "|" +
          std::to_string(dev);
   if (fl)
-    for (int v : {fl->B, fl->nqb, fl->rows, fl->d, fl->T, fl->P, fl->F, fl->slots_x, (int)fl->share_tail})
+    for (int v : {fl->B, fl->nqb, fl->rows, fl->d, fl->T, fl->P, fl->F, fl->slots_x, (int)fl->share_tail,
+                  (int)fl->by_length})
       key += "|" + std::to_string(v);
   std::lock_guard<std::mutex> lock(g_cache_mutex);
   if (auto h = g_cache.acquire(key)) {
@@ -313,7 +354,7 @@ int work_list_for(const uint8_t* masks, int n_masks, int H, int F, bool allow_sp
   HostWorkList hw = build_work_list(masks, n_masks, H, F, allow_split);
   if (fl)
     append_fwd_schedule(hw, fl->B, fl->nqb, fl->rows, fl->d, fl->T, fl->P, fl->F, fl->slots_x,
-                        fl->share_tail);
+                        fl->share_tail, fl->by_length);
   const size_t total = hw.words.size() * sizeof(int32_t);
   void* buf = nullptr;
   hipError_t e = hipMalloc(&buf, total);
@@ -506,6 +547,7 @@ int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, i
   a.cut_units = wl->cut_units;
   a.n_cut_units = wl->n_cut_units;
   a.wg_per_xcd = wl->wg_per_xcd;
+  a.unit_table = wl->unit_table;
   a.slots_per_xcd = std::max(1, slots_x);
   a.queue = queue;
   a.lse = lse;
@@ -569,7 +611,10 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
     masks = aug.data();
   }
   const int rows = ta::fwd_rows_per_workgroup(d);
-  const FwdLaunch fl{B, (int)nqb, rows, d, T, P, F, resident_slots_per_xcd(dev), true};
+  // The MM-DiT form's units differ much in length (text and global rows keep every
+  // segment, other rows a few): each XCD runs its share longest first where that
+  // changes the order and the plan splits no frame.
+  const FwdLaunch fl{B, (int)nqb, rows, d, T, P, F, resident_slots_per_xcd(dev), true, P > 0};
   PlanGuard plan(stream);
   int st = work_list_for(masks, n_masks, H, n_seg, true, dev, &plan.use, &fl);
   if (st != TA_OK) return st;
@@ -579,7 +624,7 @@ int run_fwd(const void* q, const void* k, const void* v, void* out, int B, int H
   };
   if (ws_bytes(plan.use.wl) > kMaxWorkspaceBytes || (int64_t)8 * plan.use.wl.wg_per_xcd > max_wg) {
     end_plan_use(plan.use, stream);
-    const FwdLaunch plain{B, (int)nqb, rows, d, T, P, F, fl.slots_x, false};
+    const FwdLaunch plain{B, (int)nqb, rows, d, T, P, F, fl.slots_x, false, fl.by_length};
     st = work_list_for(masks, n_masks, H, n_seg, false, dev, &plan.use, &plain);  // the same rows, not split
     if (st != TA_OK) return st;
   }

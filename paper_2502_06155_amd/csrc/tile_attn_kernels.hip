@@ -907,11 +907,12 @@ hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
   };
   using Y = std::true_type;
   using N = std::false_type;
+  const bool table = a.n_cut_units > 0 || a.unit_table;
   if (a.P > 0) {
-    if (a.n_cut_units > 0) go(Y{}, Y{});
+    if (table) go(Y{}, Y{});
     else go(Y{}, N{});
   } else {
-    if (a.n_cut_units > 0) go(N{}, Y{});
+    if (table) go(N{}, Y{});
     else go(N{}, N{});
   }
   hipError_t e = hipGetLastError();

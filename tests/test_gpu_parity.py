@@ -482,3 +482,29 @@ def test_ragged_round_in_parts(B, H, F, T, d, g, form):
         assert_lse(lse[:, hh:hh + 1], ref, f"parts-lse-h{hh}")
     # the plain entry point takes the same schedule: same bits
     assert np.array_equal(run_gpu(qb, kb, vb, mask, T, scale), got)
+
+
+def test_ragged_round_in_parts_with_empty_frames():
+    """Query frames that keep nothing (every seventh) in a launch whose XCDs end on a
+    ragged round cut into parts (tests/test_schedule.py covers the same shape): a
+    block with rows and no kept tile still runs, writing zeros and a -inf
+    log-sum-exp, wherever it falls in the schedule."""
+    B, H, F, T, d = 1, 12, 20, 700, 96
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=4242)
+    mask = om.tile_mask(F, 2, "col")
+    empty = list(range(6, F, 7))
+    mask[empty, :] = 0
+    scale = d ** -0.5
+    print(f"[case] parts with empty frames {empty}", flush=True)
+    q, k, v = to_dev(qb), to_dev(kb), to_dev(vb)
+    out = torch.full_like(q, float("nan"))
+    lse = torch.full((B, H, F * T), 12345.0, dtype=torch.float32, device="cuda")
+    ta.tile_attn_fwd_heads(q, k, v, out, B, H, F, T, d, mask, scale, lse, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    got, lse = from_dev(out), lse.cpu().numpy().astype(np.float64)
+    for f in empty:
+        rows = slice(f * T, (f + 1) * T)
+        assert np.all(got[:, :, rows] == 0), f
+        assert np.all(np.isneginf(lse[:, :, rows])), f
+    b, h, srows = sample_rows(B, H, F, T, per_frame=4, seed=7)
+    assert_parity(got[b, h, srows], oa.attention_rows(qb, kb, vb, mask, T, scale, b, h, srows), "parts-empty")

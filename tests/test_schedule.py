@@ -1,7 +1,8 @@
 """The forward launch schedule, host logic only: a C++ check compiled against the built
 library replays the schedule of several shapes and confirms every kept tile of every
 query block is computed exactly once, by a whole-block workgroup or by one of the
-parts a ragged last round is cut into."""
+parts a ragged last round is cut into, that every query block with rows runs (also one
+that keeps no tile), and that MM-DiT plans run each XCD's share longest first."""
 import os
 import re
 import shutil
@@ -30,14 +31,21 @@ def test_schedule_covers_every_tile_once(tmp_path):
     res = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
     print(res.stdout)
     assert res.returncode == 0, res.stdout + res.stderr
-    got = {m.group(1): (int(m.group(2)), int(m.group(3)), int(m.group(4)), int(m.group(5)))
-           for m in re.finditer(r"^(\S+) units (\d+) whole (\d+) parts (\d+) slots (\d+)$", res.stdout, re.M)}
-    assert len(got) == 13
+    got = {m.group(1): tuple(int(m.group(i)) for i in range(2, 7))
+           for m in re.finditer(r"^(\S+) units (\d+) whole (\d+) parts (\d+) slots (\d+) table (\d)$",
+                                res.stdout, re.M)}
+    assert len(got) == 15
     # a launch whose XCDs run whole rounds only keeps every block whole
-    assert got["93f-col"] == (8640, 8640, 0, 0)
+    assert got["93f-col"] == (8640, 8640, 0, 0, 0)
     # the GPU parity shapes are cut into parts, so those tests cover the merge
-    for name in ("gpu-a", "gpu-b", "gpu-c", "gpu-d", "gpu-e"):
+    for name in ("gpu-a", "gpu-b", "gpu-c", "gpu-d", "gpu-e", "gpu-f"):
         assert got[name][3] > 0, name
     # plans with split frames keep their pieces whole
     for name in ("sp-sym", "cog-sym"):
-        assert got[name][1] == got[name][0], name
+        assert got[name][2] == 0, name
+    # an MM-DiT plan without split frames runs longest first from a table that leaves
+    # out the text query blocks past the text's end (5 of 6 per head at 226 text
+    # tokens); with split frames (one global frame) it keeps the natural order for the
+    # kernel's persistent loop
+    assert got["cog-sym2"][4] == 1 and got["cog-sym2"][1] == got["cog-sym2"][0] - 48 * 5
+    assert got["cog-sym"][4] == 0
