@@ -34,10 +34,10 @@ struct FwdArgs {
   float c;              // > 0: |scale| * log2(e), logits in base-2 units
   uint32_t qflip;       // 0x80008000 flips the sign of q (negative scale), else 0
   uint32_t qmask;       // 0 zeroes q (scale 0: exactly uniform weights), else ~0
-  // The launch schedule (on the device): per XCD (8 of them) {first unit, whole
-  // units, part workgroups, first piece}, then per part workgroup a piece {unit, first
-  // tile, tiles, partial slot}; and per unit run in parts {unit, first partial slot,
-  // parts}. Units are (b, item, query block), query block fastest.
+  // The launch schedule (on the device): per XCD (8 of them) {first unit, contiguous
+  // whole units, table entries, first entry}, then the table entries {unit, first
+  // tile, tiles, partial slot (-1: a whole unit)}; and per unit run in parts {unit,
+  // first partial slot, parts}. Units are (b, item, query block), query block fastest.
   const int32_t* sched;
   const int32_t* cut_units;
   int n_cut_units;

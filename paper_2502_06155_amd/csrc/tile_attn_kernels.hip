@@ -296,7 +296,7 @@ struct FwdItem {
 // query blocks hold fwd_rows_per_wg<D>() rows whatever QB is: at d = 64 a block at the
 // end of a segment with at most 32 valid rows per wave runs with QB = 1, so no wave
 // computes a column block that lies wholly past the segment end.
-template <int D, bool PREFIX, int QB, bool PARTS>
+template <int D, bool PREFIX, int QB, bool TABLE>
 __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layout<PREFIX>& lay,
                                          uint16_t (&sK)[2][Shape<D>::kTileElems],
                                          uint16_t (&sV)[2][Shape<D>::kTileElems],
@@ -314,7 +314,7 @@ __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layo
   const size_t head_rows = it.head_rows;
   const uint32_t b = it.b, bh = it.bh;
   const int kbeg = it.kbeg, n_kept = it.n_kept, slot = it.slot, qb = it.qb;
-  const int part = PARTS ? it.part : -1;
+  const int part = TABLE ? it.part : -1;
   const int seg0 = it.seg0, seg_len = it.seg_len;
   [[maybe_unused]] const int F = lay.F, T = lay.T, P = lay.P;
 
@@ -364,7 +364,7 @@ __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layo
     // the text segment (index F) sorts last in a kept list
     if (n_kept > 0 && cols[kbeg + n_kept - 1] == F) n_tiles += (P + kBlockK - 1) / kBlockK - tpf;
   }
-  if constexpr (PARTS) {
+  if constexpr (TABLE) {
     if (it.nt >= 0) n_tiles = it.nt;  // a part of the kept tiles, from tile it.t0
   }
 
@@ -379,7 +379,7 @@ __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layo
     va.init(lane);
     SegmentCursor<PREFIX> cur, nxt;  // tile t (being consumed) and tile t+1 (being loaded)
     cur.start(cols + kbeg, lay);
-    if constexpr (PARTS) {
+    if constexpr (TABLE) {
       if (it.t0 > 0) cur.skip(it.t0, n_kept);
     }
     kl.load(Kh, cur.key0(), cur.nvalid(), sK[0], wave);
@@ -611,12 +611,13 @@ __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layo
 // fastest, covers the item's kept tiles for kBlockQ query rows. XCD x (the workgroups
 // with blockIdx % 8 == x; each XCD has its own L2) owns the positions 0 .. n_x - 1 of
 // its queue: positions below n_dp_x are the units start_x + pos, run whole; the
-// n_part_x after them are parts of the units that would otherwise make a ragged last
-// round of whole units, each a piece {u, first tile, tiles, partial slot}. sched holds
-// {start_x, n_dp_x, n_part_x, first piece} per XCD, then the pieces. Launches without
-// parts (PARTS false) give XCD x the contiguous units [x q + min(x, r), + q + (x < r))
-// of the n = q 8 + r units, computed in place.
-template <int D, bool PREFIX, bool PARTS>
+// n_tab_x after them are table entries {u, first tile, tiles, partial slot}: a part of
+// a unit that would otherwise make a ragged last round of whole units (slot >= 0), or
+// a whole unit (slot -1; in a longest-first schedule n_dp_x is 0 and every unit is an
+// entry). sched holds {start_x, n_dp_x, n_tab_x, first entry} per XCD, then the
+// entries. Launches without a table (TABLE false) give XCD x the contiguous units
+// [x q + min(x, r), + q + (x < r)) of the n = q 8 + r units, computed in place.
+template <int D, bool PREFIX, bool TABLE>
 __device__ __forceinline__ void fwd_unit(
     int wave, uint32_t x, int pos, const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
     const uint16_t* __restrict__ V, uint16_t* __restrict__ O, const int32_t* __restrict__ items,
@@ -631,7 +632,7 @@ __device__ __forceinline__ void fwd_unit(
   it.nt = -1;
   it.part = -1;
   uint32_t u;
-  if constexpr (!PARTS) {
+  if constexpr (!TABLE) {
     const uint32_t n = (uint32_t)B * per_b, q = n / 8, r = n % 8;
     u = x * q + min(x, r) + (uint32_t)pos;
   } else {
@@ -676,11 +677,11 @@ __device__ __forceinline__ void fwd_unit(
   // the tile loop makes the register allocator spill the main one.
   if constexpr (fwd_q_blocks<D>() == 2 && D == 64) {
     if (it.seg_len - it.qb * kBlockQ <= kWaves * 32) {
-      fwd_rows<D, PREFIX, 1, PARTS>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip, qmask);
+      fwd_rows<D, PREFIX, 1, TABLE>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip, qmask);
       return;
     }
   }
-  fwd_rows<D, PREFIX, fwd_q_blocks<D>(), PARTS>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip,
+  fwd_rows<D, PREFIX, fwd_q_blocks<D>(), TABLE>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip,
                                                 qmask);
 }
 
@@ -716,7 +717,7 @@ struct FwdKernelArgs {
 // counters start at zero; the last workgroup to finish (counted in queue[8]) sets all
 // nine back to zero for the next launch on the same queue. No workgroup ever waits
 // for another.
-template <int D, bool PREFIX, bool PARTS, bool PERSIST>
+template <int D, bool PREFIX, bool TABLE, bool PERSIST>
 __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(const FwdKernelArgs args) {
   using Sh = Shape<D>;
   __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
@@ -726,7 +727,7 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(const FwdKer
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   // Queue positions of XCD y.
   auto positions = [](uint32_t y, int B, int n_items, int nqb, const int32_t* sched) {
-    if constexpr (!PARTS) {
+    if constexpr (!TABLE) {
       const uint32_t n = (uint32_t)B * (uint32_t)n_items * (uint32_t)nqb;
       return (int)(n / 8 + (y < n % 8 ? 1u : 0u));
     } else {
@@ -736,7 +737,7 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(const FwdKer
   if constexpr (!PERSIST) {
     const int pos = (int)(blockIdx.x / 8);
     if (pos >= positions(x, args.B, args.n_items, args.nqb, args.sched)) return;
-    fwd_unit<D, PREFIX, PARTS>(wave, x, pos, args.Q, args.K, args.V, args.O, args.items, args.cols,
+    fwd_unit<D, PREFIX, TABLE>(wave, x, pos, args.Q, args.K, args.V, args.O, args.items, args.cols,
                                args.n_items, args.B, args.H, args.F, args.T, PREFIX ? args.P : 0, args.nqb,
                                args.sched, args.ws_o, args.ws_lse, args.lse, args.ws_parts, args.c, args.qflip,
                                args.qmask, sK, sV);
@@ -765,7 +766,7 @@ __global__ __launch_bounds__(kThreads, 2) void tile_attn_fwd_kernel(const FwdKer
       __syncthreads();
       const int pos = __builtin_amdgcn_readfirstlane(s_pos[round & 1]);
       if (pos >= positions(x, ap->B, ap->n_items, ap->nqb, ap->sched)) break;
-      fwd_unit<D, PREFIX, PARTS>(wave, x, pos, ap->Q, ap->K, ap->V, ap->O, ap->items, ap->cols,
+      fwd_unit<D, PREFIX, TABLE>(wave, x, pos, ap->Q, ap->K, ap->V, ap->O, ap->items, ap->cols,
                                  ap->n_items, ap->B, ap->H, ap->F, ap->T, PREFIX ? ap->P : 0, ap->nqb,
                                  ap->sched, ap->ws_o, ap->ws_lse, ap->lse, ap->ws_parts, ap->c, ap->qflip,
                                  ap->qmask, sK, sV);
@@ -893,17 +894,17 @@ hipError_t launch_d(const FwdArgs& a, hipStream_t stream) {
   // units only where the schedule has some.
   const bool persist = a.queue != nullptr && a.P > 0 && D == 64;
   const dim3 grid(8u * (uint32_t)(persist ? std::min(a.wg_per_xcd, a.slots_per_xcd) : a.wg_per_xcd));
-  auto go = [&](auto prefix, auto parts) {
-    constexpr bool kPrefix = decltype(prefix)::value, kParts = decltype(parts)::value;
+  auto go = [&](auto prefix, auto table_c) {
+    constexpr bool kPrefix = decltype(prefix)::value, kTable = decltype(table_c)::value;
     const FwdKernelArgs ka{a.q,      a.k,   a.v,        a.out,   a.items,         a.cols,
                            a.sched,  a.ws_o, a.ws_lse,  a.lse,   a.ws_parts,      a.queue,
                            (int)grid.x, a.n_items, a.B, a.H,    a.F,             a.T,
                            kPrefix ? a.P : 0, nqb, a.c, a.qflip, a.qmask};
     if (kPrefix && D == 64 && persist)
-      hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kParts, kPrefix && D == 64>), grid, dim3(kThreads), 0,
+      hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kTable, kPrefix && D == 64>), grid, dim3(kThreads), 0,
                          stream, ka);
     else
-      hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kParts, false>), grid, dim3(kThreads), 0, stream, ka);
+      hipLaunchKernelGGL((tile_attn_fwd_kernel<D, kPrefix, kTable, false>), grid, dim3(kThreads), 0, stream, ka);
   };
   using Y = std::true_type;
   using N = std::false_type;
