@@ -288,13 +288,12 @@ __device__ __forceinline__ void dq_scores(const f32x16& s, const f32x16& dp, flo
   }
 }
 
+// The query-side pass over one work unit (b, item, query block).
 template <int D, bool PREFIX>
-__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a, int nqb) {
+__device__ __forceinline__ void dq_unit(const BwdArgs& a, int nqb, uint32_t work,
+                                        uint16_t (&sK)[2][BShape<D>::kTileElems],
+                                        uint16_t (&sV)[2][BShape<D>::kTileElems]) {
   using Sh = BShape<D>;
-  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
-
-  const uint32_t work = xcd_remap(blockIdx.x, a.n_wg_q);
   const uint32_t per_b = (uint32_t)a.n_items_q * (uint32_t)nqb;
   const uint32_t b = work / per_b;
   const uint32_t rem = work - b * per_b;
@@ -424,6 +423,16 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a,
   }
 }
 
+// One workgroup per unit; the ids the hardware sends to one XCD cover a contiguous
+// range of units.
+template <int D, bool PREFIX>
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dq_kernel(const BwdArgs a, int nqb) {
+  using Sh = BShape<D>;
+  __shared__ __attribute__((aligned(1024))) uint16_t sK[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sV[2][Sh::kTileElems];
+  dq_unit<D, PREFIX>(a, nqb, xcd_remap(blockIdx.x, a.n_wg_q), sK, sV);
+}
+
 // fn(integral_constant<int, i>) for i = 0 .. N-1, in order.
 template <int N, int I = 0, typename Fn>
 __device__ __forceinline__ void static_for(Fn&& fn) {
@@ -435,16 +444,14 @@ __device__ __forceinline__ void static_for(Fn&& fn) {
 
 // ---------------------------------------------------------------------------
 // dk/dv pass.
+// The key-side pass over one work unit (b, item of the transposed plan, key block).
 template <int D, bool PREFIX, int MODE>
-__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs a, int nkb) {
+__device__ __forceinline__ void dkdv_unit(const BwdArgs& a, int nkb, uint32_t work,
+                                          uint16_t (&sQ)[2][BShape<D>::kTileElems],
+                                          uint16_t (&sG)[2][BShape<D>::kTileElems],
+                                          float (&sL)[2][kBlockK], float (&sD)[2][kBlockK]) {
   constexpr bool kWantDv = MODE != kDkOnly, kWantDk = MODE != kDvOnly;
   using Sh = BShape<D>;
-  __shared__ __attribute__((aligned(1024))) uint16_t sQ[2][Sh::kTileElems];
-  __shared__ __attribute__((aligned(1024))) uint16_t sG[2][Sh::kTileElems];
-  __shared__ __attribute__((aligned(256))) float sL[2][kBlockK];
-  __shared__ __attribute__((aligned(256))) float sD[2][kBlockK];
-
-  const uint32_t work = xcd_remap(blockIdx.x, a.n_wg_k);
   const uint32_t per_b = (uint32_t)a.n_items_k * (uint32_t)nkb;
   const uint32_t b = work / per_b;
   const uint32_t rem = work - b * per_b;
@@ -685,6 +692,19 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs 
       if constexpr (kWantDv) store_row_f32<D>(a.ws_dv + prow * D, dv, 1.f, hf);
     }
   }
+}
+
+// One workgroup per unit, as in the query-side pass. (The unit body is a separate
+// function in both passes; compiled so, the d = 128 dK pass fits 256 VGPRs without the
+// two spilled registers it had as one kernel body, 1.2% faster.)
+template <int D, bool PREFIX, int MODE>
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_dkdv_kernel(const BwdArgs a, int nkb) {
+  using Sh = BShape<D>;
+  __shared__ __attribute__((aligned(1024))) uint16_t sQ[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(1024))) uint16_t sG[2][Sh::kTileElems];
+  __shared__ __attribute__((aligned(256))) float sL[2][kBlockK];
+  __shared__ __attribute__((aligned(256))) float sD[2][kBlockK];
+  dkdv_unit<D, PREFIX, MODE>(a, nkb, xcd_remap(blockIdx.x, a.n_wg_k), sQ, sG, sL, sD);
 }
 
 // ---------------------------------------------------------------------------
