@@ -46,15 +46,15 @@
  *     frame, that round's query blocks are cut into parts over their kept tiles,
  *     n_parts * R * (d + 4) * 4 bytes (R = 256 query rows per block, 128 at
  *     d = 128; n_parts is at most 16 per block cut, and zero when the launch
- *     fills whole rounds). The MM-DiT forward at d = 64 also uses 256 bytes of
- *     work-queue counters, allocated and zeroed (synchronously) by the first such
- *     call on a stream; every call leaves them zero. The workspace is held per
- *     (device, stream). A call that
- *     needs more allocates a larger one (at least 1.5 times the size) and keeps
- *     the old one allocated until process exit, so no enqueued work ever sees
- *     its workspace freed and growing never waits for the stream. Later calls
- *     that fit allocate nothing and do not synchronise, so a warmed-up call can
- *     be captured in a HIP graph.
+ *     fills whole rounds). An MM-DiT forward at d = 64 whose plan splits frames
+ *     also uses 256 bytes of work-queue counters, allocated and zeroed
+ *     (synchronously) by the first such call on a stream; every call leaves them
+ *     zero. The workspace is held per (device, stream). A call that needs more
+ *     allocates a larger one (at least 1.5 times the size) and keeps the old one
+ *     allocated until process exit, so no enqueued work ever sees its workspace
+ *     freed and growing never waits for the stream. Later calls that fit allocate
+ *     nothing and do not synchronise, so a warmed-up call can be captured in a
+ *     HIP graph.
  *   - The workspace and the counters are found by the stream handle: calls on
  *     one stream share them in stream order, calls on different live streams
  *     never share them. Two cases do share them with work that may still run,
