@@ -522,7 +522,6 @@ int enqueue_fwd(const void* q, const void* k, const void* v, void* out, int B, i
                 float* lse, void* stream, int* queue, int slots_x) {
   const DeviceWorkList* wl = &plan;
   const int L = std::max(T, P);
-  const int64_t nqb = (L + ta::fwd_rows_per_workgroup(d) - 1) / ta::fwd_rows_per_workgroup(d);
   hipError_t e;
   ta::FwdArgs a;
   a.q = static_cast<const uint16_t*>(q);
