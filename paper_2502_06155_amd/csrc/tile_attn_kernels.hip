@@ -10,7 +10,9 @@
 //   each wave owns 64 rows as two 32-query column blocks (128 rows and one block
 //   at d = 128, see fwd_q_blocks; at d = 64 a block at the end of a frame with at
 //   most 32 valid rows per wave also runs one column block per wave, see
-//   fwd_rows). Query blocks are frame aligned, so every row of
+//   fwd_rows; a block with at most 32 valid rows in all runs on two waves that
+//   split the keys of every tile, see fwd_tail_rows). Query blocks are frame
+//   aligned, so every row of
 //   a workgroup shares one kept list. With a text prefix (the MM-DiT form) the text
 //   is one more segment, see Layout. Workgroup ids are
 //   remapped so that each XCD (8 per MI355X, each with its own L2) receives a
@@ -292,6 +294,72 @@ struct FwdItem {
   int t0, nt, part;
 };
 
+// Epilogue of a wave's QB column blocks, whose first row (within the segment) is
+// row0: normalise; a whole frame rounds to bf16 (RNE) into out, a piece of a split
+// frame stores O/l in fp32 and its base-2 log-sum-exp log2(sum_t 2^(c s_t)) =
+// c m_ref + log2(l) for the merge, and a part of the kept tiles (part >= 0) stores
+// the same to its own slot. 4 consecutive d per access. The lane's rows are derived
+// from a lane id read here, so that nothing lane-dependent from before the tile loop
+// has to stay live across it.
+template <int D, bool PREFIX, int QB>
+__device__ __forceinline__ void store_rows(const FwdItem& it, int row0, int part,
+                                           const f32x16 (&o)[QB][Shape<D>::kDBlocks], const float (&m_ref)[QB],
+                                           const float (&l_run)[QB], float c, int T, int P, float* __restrict__ lse,
+                                           float* __restrict__ ws_o, float* __restrict__ ws_lse,
+                                           float* __restrict__ ws_parts) {
+  using Sh = Shape<D>;
+  constexpr int kBlockQ = fwd_rows_per_wg<D>();
+  const int seg0 = it.seg0, seg_len = it.seg_len, slot = it.slot, qb = it.qb;
+  // The row offsets below are formed here, after the tile loop: values derived from
+  // them are not worth a scalar register across the loop.
+  asm volatile("" : "+s"(T), "+s"(P));
+  int lane_e;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane_e));
+  const int hf_e = lane_e >> 5;
+  const int qrow0_e = row0 + (lane_e & 31);
+#pragma unroll
+  for (int qs = 0; qs < QB; ++qs) {
+    const float l_tot = pair_sum(l_run[qs]);
+    const int qrow = qrow0_e + 32 * qs;
+    if (qrow < seg_len) {
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      if (slot < 0 && part < 0) {
+        uint16_t* op = it.Oh + ((size_t)seg0 + qrow) * D;
+#pragma unroll
+        for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
+                       o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
+            const bf16x4 y = __builtin_convertvector(x, bf16x4);
+            *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf_e) = __builtin_bit_cast(u32x2, y);
+          }
+        if (lse && hf_e == 0)
+          lse[(size_t)it.bh * it.head_rows + seg0 + qrow] =
+              l_tot > 0.f ? (m_ref[qs] * c + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f
+                          : -INFINITY;
+      } else {
+        // A part of the kept tiles (part >= 0) goes to its own slot of kBlockQ rows of
+        // D + 4 floats (O/l, then the log-sum-exp), a piece of a split frame (slot >= 0)
+        // to the frame's partial rows.
+        const int slot_rows = PREFIX ? max(T, P) : T;  // rows per (slot, batch entry)
+        const size_t prow = part >= 0 ? (size_t)part * kBlockQ + (qrow - qb * kBlockQ)
+                                    : ((size_t)slot * it.B + it.b) * slot_rows + qrow;
+        float* op = part >= 0 ? ws_parts + prow * (D + 4) : ws_o + prow * D;
+#pragma unroll
+        for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
+                             o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
+            *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * i + 4 * hf_e) = x;
+          }
+        if (hf_e == 0) *(part >= 0 ? op + D : ws_lse + prow) = m_ref[qs] * c + __builtin_amdgcn_logf(l_tot);
+      }
+    }
+  }
+}
+
 // The rows of one workgroup with QB 32-query column blocks per wave. The grid's
 // query blocks hold fwd_rows_per_wg<D>() rows whatever QB is: at d = 64 a block at the
 // end of a segment with at most 32 valid rows per wave runs with QB = 1, so no wave
@@ -309,11 +377,8 @@ __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layo
   const uint16_t* Qh = it.Qh;
   const uint16_t* Kh = it.Kh;
   const uint16_t* Vh = it.Vh;
-  uint16_t* Oh = it.Oh;
   const int32_t* cols = it.cols;
-  const size_t head_rows = it.head_rows;
-  const uint32_t b = it.b, bh = it.bh;
-  const int kbeg = it.kbeg, n_kept = it.n_kept, slot = it.slot, qb = it.qb;
+  const int kbeg = it.kbeg, n_kept = it.n_kept, qb = it.qb;
   const int part = TABLE ? it.part : -1;
   const int seg0 = it.seg0, seg_len = it.seg_len;
   [[maybe_unused]] const int F = lay.F, T = lay.T, P = lay.P;
@@ -554,57 +619,152 @@ __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layo
     }
   }
 
-  // Epilogue: normalise; a whole frame rounds to bf16 (RNE) into out, a piece of
-  // a split frame stores O/l in fp32 and its base-2 log-sum-exp
-  // log2(sum_t 2^(c s_t)) = c m_ref + log2(l) for the merge. 4 consecutive d per
-  // access.
-  // The lane's rows are derived again from a lane id read here, so that nothing
-  // lane-dependent from before the tile loop has to stay live across it.
-  int lane_e;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane_e));
-  const int hf_e = lane_e >> 5;
-  const int qrow0_e = qb * kBlockQ + wave * kWaveQ + (lane_e & 31);
+  store_rows<D, PREFIX, QB>(it, qb * kBlockQ + wave * kWaveQ, part, o, m_ref, l_run, c, T, P, lse, ws_o,
+                            ws_lse, ws_parts);
+}
+
+// A query block with at most 32 valid rows (the short last block of a segment, such
+// as the 16 rows left at T = 3600): one 32-query column block, shared by waves 0 and
+// 1, which take the two 32-key halves of every tile; waves 2 and 3 only load tiles.
+// Wave 1's softmax state (reference, sum, O^T) then joins wave 0's through LDS and
+// wave 0 stores the rows. Each tile costs an active wave a quarter of the matrix and
+// vector work of a full block's wave (half at d = 128, whose full blocks have one
+// column block per wave), so the block frees its workgroup slot early instead of
+// holding it for one wave's whole pass over the tiles.
+template <int D, bool PREFIX, bool TABLE>
+__device__ __forceinline__ void fwd_tail_rows(int wave, const FwdItem& it, const Layout<PREFIX>& lay,
+                                              uint16_t (&sK)[2][Shape<D>::kTileElems],
+                                              uint16_t (&sV)[2][Shape<D>::kTileElems],
+                                              float* __restrict__ ws_o, float* __restrict__ ws_lse,
+                                              float* __restrict__ lse, float* __restrict__ ws_parts, float c,
+                                              uint32_t qflip, uint32_t qmask) {
+  using Sh = Shape<D>;
+  constexpr int kBlockQ = fwd_rows_per_wg<D>();
+  const int32_t* cols = it.cols;
+  const int kbeg = it.kbeg, n_kept = it.n_kept, qb = it.qb;
+  const int part = TABLE ? it.part : -1;
+  const int seg0 = it.seg0, seg_len = it.seg_len;
+  [[maybe_unused]] const int F = lay.F, T = lay.T, P = lay.P;
+
+  int lane;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+  const int n = lane & 31, hf = lane >> 5;
+  const bool wave_active = wave < 2;  // wave w takes keys 32 w .. 32 w + 31 of every tile
+
+  bf16x8 qf[1][Sh::kChunks];
+  {
+    const int qrow = qb * kBlockQ + n;
+    const uint16_t* qp = it.Qh + ((size_t)seg0 + qrow) * D + 8 * hf;
 #pragma unroll
-  for (int qs = 0; qs < QB; ++qs) {
-    const float l_tot = pair_sum(l_run[qs]);
-    const int qrow = qrow0_e + 32 * qs;
-    if (qrow < seg_len) {
-      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      if (slot < 0 && part < 0) {
-        uint16_t* op = Oh + ((size_t)seg0 + qrow) * D;
-#pragma unroll
-        for (int mb = 0; mb < Sh::kDBlocks; ++mb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
-                       o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
-            const bf16x4 y = __builtin_convertvector(x, bf16x4);
-            *reinterpret_cast<u32x2*>(op + 32 * mb + 8 * i + 4 * hf_e) = __builtin_bit_cast(u32x2, y);
-          }
-        if (lse && hf_e == 0)
-          lse[(size_t)bh * head_rows + seg0 + qrow] =
-              l_tot > 0.f ? (m_ref[qs] * c + __builtin_amdgcn_logf(l_tot)) * 0.69314718055994531f
-                          : -INFINITY;
-      } else {
-        // A part of the kept tiles (part >= 0) goes to its own slot of kBlockQ rows of
-        // D + 4 floats (O/l, then the log-sum-exp), a piece of a split frame (slot >= 0)
-        // to the frame's partial rows.
-        const int slot_rows = PREFIX ? max(T, P) : T;  // rows per (slot, batch entry)
-        const size_t prow = part >= 0 ? (size_t)part * kBlockQ + (qrow - qb * kBlockQ)
-                                    : ((size_t)slot * it.B + b) * slot_rows + qrow;
-        float* op = part >= 0 ? ws_parts + prow * (D + 4) : ws_o + prow * D;
-#pragma unroll
-        for (int mb = 0; mb < Sh::kDBlocks; ++mb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const f32x4 x = {o[qs][mb][4 * i + 0] * inv, o[qs][mb][4 * i + 1] * inv,
-                             o[qs][mb][4 * i + 2] * inv, o[qs][mb][4 * i + 3] * inv};
-            *reinterpret_cast<f32x4*>(op + 32 * mb + 8 * i + 4 * hf_e) = x;
-          }
-        if (hf_e == 0) *(part >= 0 ? op + D : ws_lse + prow) = m_ref[qs] * c + __builtin_amdgcn_logf(l_tot);
-      }
+    for (int cc = 0; cc < Sh::kChunks; ++cc) {
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (qrow < seg_len) x = (load16(qp + 16 * cc) & qmask) ^ qflip;
+      qf[0][cc] = as_bf16x8(x);
     }
   }
+  f32x16 o[1][Sh::kDBlocks];
+#pragma unroll
+  for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[0][mb] = f32x16{};
+  float m_ref[1] = {-INFINITY}, l_run[1] = {0.f};
+  const float lazy = exp2f(kLazyLog2);
+
+  const int tpf = (T + kBlockK - 1) / kBlockK;
+  int n_tiles = n_kept * tpf;
+  if constexpr (PREFIX) {
+    if (n_kept > 0 && cols[kbeg + n_kept - 1] == F) n_tiles += (P + kBlockK - 1) / kBlockK - tpf;
+  }
+  if constexpr (TABLE) {
+    if (it.nt >= 0) n_tiles = it.nt;
+  }
+
+  if (n_tiles > 0) {
+    TileLoader<D, true> kl;
+    TileLoader<D, false> vl;
+    kl.init(wave, lane);
+    vl.init(wave, lane);
+    KAddr<D> ka;
+    VAddr<D> va;
+    ka.init(n, hf);
+    va.init(lane);
+    SegmentCursor<PREFIX> cur, nxt;
+    cur.start(cols + kbeg, lay);
+    if constexpr (TABLE) {
+      if (it.t0 > 0) cur.skip(it.t0, n_kept);
+    }
+    kl.load(it.Kh, cur.key0(), cur.nvalid(), sK[0], wave);
+    vl.load(it.Vh, cur.key0(), cur.nvalid(), sV[0], wave);
+    nxt = cur;
+    nxt.advance(n_kept);
+    wait_tile_loads();
+    __syncthreads();
+
+    auto tile_step = [&](auto bufc, int t) {
+      constexpr int buf = decltype(bufc)::value;
+      if (t + 1 < n_tiles) {
+        kl.load(it.Kh, nxt.key0(), nxt.nvalid(), sK[buf ^ 1], wave);
+        vl.load(it.Vh, nxt.key0(), nxt.nvalid(), sV[buf ^ 1], wave);
+      }
+      const int nvalid = cur.nvalid();
+      // A half with no valid key (the second half of a frame's last tile of at most
+      // 32 keys) is skipped: its weights would be NaN while the reference is -inf.
+      if (wave_active && 32 * wave < nvalid) {
+        f32x16 s[1];
+        bf16x8 p[1][2];
+        qk_block<D, 1>(sK[buf], qf, ka, wave, s);
+        if (nvalid < 32 * (wave + 1)) mask_tail(s[0], wave, hf, nvalid);
+        float ls = block_weights(s[0], c, m_ref[0] * c, p[0]);
+        // As in the full blocks: the weights are kept when every lane's sum is at
+        // most 2^kLazyLog2, else the reference is raised and the block redone.
+        if (__builtin_amdgcn_ballot_w64(!(ls <= lazy)) != 0) {
+          const float m_new = fmaxf(m_ref[0], pair_max(block_max(s[0])));
+          const float alpha = fast_exp2((m_ref[0] - m_new) * c);
+          l_run[0] *= alpha;
+#pragma unroll
+          for (int mb = 0; mb < Sh::kDBlocks; ++mb) o[0][mb] *= alpha;
+          m_ref[0] = m_new;
+          ls = block_weights(s[0], c, m_new * c, p[0]);
+        }
+        l_run[0] += ls;
+        pv_block<D, 1>(sV[buf], p, va, wave, o);
+      }
+      cur = nxt;
+      nxt.advance(n_kept);
+      wait_tile_loads();
+      __syncthreads();
+    };
+    for (int t = 0; t < n_tiles; t += 2) {
+      tile_step(std::integral_constant<int, 0>{}, t);
+      if (t + 1 < n_tiles) tile_step(std::integral_constant<int, 1>{}, t + 1);
+    }
+
+    // Every wave has passed the last tile's barrier and no load is in flight, so the
+    // K buffers hold wave 1's state: value i of lane l at float i * 64 + l.
+    float* xs = reinterpret_cast<float*>(&sK[0][0]);
+    if (wave == 1) {
+      xs[lane] = m_ref[0];
+      xs[64 + lane] = l_run[0];
+#pragma unroll
+      for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) xs[(2 + 16 * mb + r) * 64 + lane] = o[0][mb][r];
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // Wave 0 saw the first half of every tile, which always holds a valid key, so
+      // its reference is finite; wave 1's is -inf if it saw none (weight 0 below).
+      const float m1 = xs[lane];
+      const float m_new = fmaxf(m_ref[0], m1);
+      const float a0 = fast_exp2((m_ref[0] - m_new) * c), a1 = fast_exp2((m1 - m_new) * c);
+      l_run[0] = l_run[0] * a0 + xs[64 + lane] * a1;
+#pragma unroll
+      for (int mb = 0; mb < Sh::kDBlocks; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[0][mb][r] = o[0][mb][r] * a0 + xs[(2 + 16 * mb + r) * 64 + lane] * a1;
+      m_ref[0] = m_new;
+    }
+  }
+  if (wave == 0)
+    store_rows<D, PREFIX, 1>(it, qb * kBlockQ, part, o, m_ref, l_run, c, T, P, lse, ws_o, ws_lse, ws_parts);
 }
 
 // One unit of work. Logical unit u = (batch entry b, item i, query block qb), qb
@@ -672,6 +832,17 @@ __device__ __forceinline__ void fwd_unit(
   it.Vh = V + it.bh * head_elems;
   it.Oh = O + it.bh * head_elems;
 
+  // A query block at the end of a segment with at most 32 valid rows runs on two
+  // waves that split the keys of every tile. Not in the d = 96 kernels with a text
+  // prefix or a unit table: their epilogues keep more scalars live across the main
+  // tile loop, and with this path as well one of them spills to a vector register,
+  // which pushes a loader offset of the loop (at 256 VGPRs) into scratch memory.
+  if constexpr (D != 96 || (!PREFIX && !TABLE)) {
+    if (it.seg_len - it.qb * kBlockQ <= 32) {
+      fwd_tail_rows<D, PREFIX, TABLE>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip, qmask);
+      return;
+    }
+  }
   // A query block at the end of a segment with at most 32 valid rows per wave runs
   // with one column block per wave. Only at d = 64: at d = 96 the second instance of
   // the tile loop makes the register allocator spill the main one.

@@ -5,7 +5,8 @@
 // runs (whole or in parts, also one that keeps no tile), every partial slot belongs to
 // one unit, MM-DiT plans list their whole units longest first, and the per-XCD
 // workgroup counts fit the grid. Prints one line per shape:
-// "<name> units U whole W parts P slots S table 0|1".
+// "<name> units U whole W parts P slots S table 0|1 short C", C the units cut into
+// parts whose query block holds at most 32 rows.
 #include <cstdio>
 #include <cstdlib>
 #include <map>
@@ -104,8 +105,14 @@ int check(const char* name, int B, int H, int F, int T, int P, int d, int g, int
     for (int s = cut[3 * k + 1]; s < cut[3 * k + 1] + cut[3 * k + 2]; ++s, ++slots)
       if (slot_unit.count(s) == 0 || slot_unit[s] != cut[3 * k]) return std::printf("%s: slot of another unit\n", name), 1;
   if (slots != hw.n_part_slots || (int)slot_unit.size() != hw.n_part_slots) return std::printf("%s: slot count\n", name), 1;
-  std::printf("%s units %ld whole %ld parts %ld slots %d table %d\n", name, n, whole, parts, hw.n_part_slots,
-              (int)hw.unit_table);
+  int cut_short = 0;  // units cut into parts whose query block holds at most 32 rows
+  for (int k = 0; k < hw.n_cut_units; ++k) {
+    const int32_t* it = items + 5 * ((cut[3 * k] % per_b) / nqb);
+    const int seg_len = (P > 0 && it[1] == F) ? P : T;
+    if (seg_len - (int)(cut[3 * k] % nqb) * rows <= 32) ++cut_short;
+  }
+  std::printf("%s units %ld whole %ld parts %ld slots %d table %d short %d\n", name, n, whole, parts,
+              hw.n_part_slots, (int)hw.unit_table, cut_short);
   return 0;
 }
 
@@ -131,5 +138,8 @@ int main() {
   bad |= check("gpu-e", 1, 12, 9, 1350, 226, 64, 1, TA_MASK_SYM);
   // query frames that keep nothing, some of them in the ragged round cut into parts
   bad |= check("gpu-f", 1, 12, 20, 700, 0, 96, 2, TA_MASK_COL, 7);
+  // short last query blocks (16 rows) among the units cut into parts
+  bad |= check("gpu-g", 1, 32, 6, 528, 0, 64, 1, TA_MASK_COL);
+  bad |= check("gpu-h", 1, 20, 6, 528, 0, 128, 1, TA_MASK_COL);
   return bad;
 }

@@ -159,6 +159,24 @@ def test_mmdit_ragged_round_in_parts():
         assert_lse(lse[:, hh:hh + 1], ref_lse, f"mmdit-parts-lse-h{hh}")
 
 
+@pytest.mark.parametrize("T,P", [(272, 20), (528, 3)])
+def test_mmdit_short_blocks_in_work_loop(T, P):
+    """Query blocks of at most 32 rows (the whole text, and each frame's 16-row last
+    block) in the persistent work loop of a split MM-DiT plan at d = 64: their two
+    waves pass one wave's softmax state to the other through the LDS that the next
+    unit's tile loads then reuse. Every row and the log-sum-exp against the oracle."""
+    B, H, F, d = 1, 4, 10, 64
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=T + P, prefix=P)
+    mask = om.tile_mask(F, 1, "sym")
+    aug = np.ones((F + 1, F + 1), np.uint8)
+    aug[:F, :F] = mask
+    assert ta.tile_attn_plan(aug)[1] > 0  # split frames: the persistent loop runs
+    print(f"[case] mmdit short blocks T={T} P={P}", flush=True)
+    got, lse = run_mmdit(qb, kb, vb, mask, T, P, d ** -0.5)
+    assert_parity(got, ommd.attention_mmdit(qb, kb, vb, mask, T, P, d ** -0.5), f"short-T{T}-P{P}")
+    assert_lse(lse, ommd.attention_mmdit_lse(qb, kb, mask, T, P, d ** -0.5), f"short-T{T}-P{P}")
+
+
 def test_mmdit_work_queue_in_graph_and_between_calls():
     """The MM-DiT form at d = 64 with split frames runs the kernel's persistent work
     loop, whose queue counters (per stream) every launch must leave at zero: eager

@@ -221,10 +221,11 @@ def test_full_size_sampled(name, form, g):
 
 
 def test_last_query_block_with_idle_waves():
-    """At T = 3600 the last query block of each frame holds 16 rows, so three of its
-    four waves have no rows and only help load tiles. Those waves must not
-    overwrite a K buffer that the others still read; every row of the last blocks
-    of all frames and heads is compared, at a head count that fills the GPU."""
+    """At T = 3600 the last query block of each frame holds 16 rows: two of its four
+    waves split the keys of every tile and the other two only help load tiles. No
+    wave may overwrite a K buffer that the others still read, nor the LDS that
+    carries one wave's softmax state to the other; every row of the last blocks of
+    all frames and heads is compared, at a head count that fills the GPU."""
     B, H, F, T, d = 1, 24, 3, 3600, 96
     qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=21)
     mask = om.tile_mask(F, 1, "col")
@@ -237,9 +238,9 @@ def test_last_query_block_with_idle_waves():
 
 
 def test_d64_tail_blocks_full_size():
-    """At d = 64 a frame's last query block whose rows fit 32 per wave (16 rows at
-    T = 3600) runs one 32-row column block per wave; every row of the last blocks of
-    all frames is compared, at a head count that fills the GPU."""
+    """At d = 64 a frame's last query block of 16 rows (T = 3600) runs on two waves
+    that split the keys of every tile; every row of the last blocks of all frames is
+    compared, at a head count that fills the GPU."""
     B, H, F, T, d = 1, 24, 3, 3600, 64
     qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=22)
     mask = om.tile_mask(F, 1, "col")
@@ -253,14 +254,38 @@ def test_d64_tail_blocks_full_size():
 
 @pytest.mark.parametrize("T", [272, 356])
 def test_d64_tail_blocks_of_split_frames(T):
-    """d = 64 tail blocks (16 or 100 valid rows after a full 256-row block) in the
-    pieces of split heavy frames, which write fp32 partials from the one-column-block
-    epilogue before the merge; every row is compared with the oracle."""
+    """d = 64 tail blocks (16 or 100 valid rows after a full 256-row block: keys split
+    over two waves, or one column block per wave) in the pieces of split heavy frames,
+    which write fp32 partials before the merge; every row is compared with the oracle."""
     B, H, F, d = 1, 2, 10, 64
     qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=23)
     mask = om.tile_mask(F, 1, "sym")
     assert ta.tile_attn_plan(mask)[1] > 0
     full_check(qb, kb, vb, mask, T, d ** -0.5, f"d64-tail-split-T{T}")
+
+
+SHORT_CASES = [  # (d, T): a last query block of 1 .. 32 rows; T mod 64 sets the last key tile
+    (64, 272), (64, 288), (96, 257), (96, 272), (96, 287), (96, 288), (128, 144), (128, 160), (128, 276),
+]
+
+
+@pytest.mark.parametrize("form", ["col", "sym"])
+@pytest.mark.parametrize("d,T", SHORT_CASES)
+def test_short_last_query_blocks(d, T, form):
+    """A segment's last query block with at most 32 valid rows runs on two waves, each
+    taking one 32-key half of every tile; the second wave's softmax state joins the
+    first's through LDS. The last key tile of a frame holds 16, 31 or 32 keys here, so
+    the second half is empty or partly masked; with sym masks the heavy frames are
+    split and the short blocks write partials. Every row and the log-sum-exp against
+    the oracle."""
+    B, H, F = 1, 3, 7
+    qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=T * 3 + d)
+    mask = om.tile_mask(F, 2, form)
+    scale = d ** -0.5
+    print(f"[case] short last block d={d} T={T} {form}", flush=True)
+    got, lse = run_gpu_heads(qb, kb, vb, mask, T, scale)
+    assert_parity(got, oa.attention(qb, kb, vb, mask, T, scale), f"short-d{d}-T{T}-{form}")
+    assert_lse(lse, oa.attention_lse(qb, kb, mask, T, scale), f"short-lse-d{d}-T{T}-{form}")
 
 
 # ---- split heavy query frames (partial results merged by log-sum-exp) -----------------
@@ -461,6 +486,9 @@ PART_CASES = [  # (B, H, F, T, d, g, form): each XCD's last round is cut into pa
     (1, 12, 20, 700, 96, 2, "col"),
     (1, 32, 6, 700, 96, 1, "sym"),
     (1, 8, 11, 700, 128, 1, "col"),
+    # 16-row last query blocks among the parts (keys split over two waves)
+    (1, 32, 6, 528, 64, 1, "col"),
+    (1, 20, 6, 528, 128, 1, "col"),
 ]
 
 

@@ -31,15 +31,18 @@ def test_schedule_covers_every_tile_once(tmp_path):
     res = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
     print(res.stdout)
     assert res.returncode == 0, res.stdout + res.stderr
-    got = {m.group(1): tuple(int(m.group(i)) for i in range(2, 7))
-           for m in re.finditer(r"^(\S+) units (\d+) whole (\d+) parts (\d+) slots (\d+) table (\d)$",
+    got = {m.group(1): tuple(int(m.group(i)) for i in range(2, 8))
+           for m in re.finditer(r"^(\S+) units (\d+) whole (\d+) parts (\d+) slots (\d+) table (\d) short (\d+)$",
                                 res.stdout, re.M)}
-    assert len(got) == 15
+    assert len(got) == 17
     # a launch whose XCDs run whole rounds only keeps every block whole
-    assert got["93f-col"] == (8640, 8640, 0, 0, 0)
+    assert got["93f-col"] == (8640, 8640, 0, 0, 0, 0)
     # the GPU parity shapes are cut into parts, so those tests cover the merge
-    for name in ("gpu-a", "gpu-b", "gpu-c", "gpu-d", "gpu-e", "gpu-f"):
+    for name in ("gpu-a", "gpu-b", "gpu-c", "gpu-d", "gpu-e", "gpu-f", "gpu-g", "gpu-h"):
         assert got[name][3] > 0, name
+    # among them, short last query blocks (16 rows, two waves splitting the keys)
+    for name in ("gpu-g", "gpu-h"):
+        assert got[name][5] > 0, name
     # plans with split frames keep their pieces whole
     for name in ("sp-sym", "cog-sym"):
         assert got[name][2] == 0, name
