@@ -10,9 +10,9 @@
 //   each wave owns 64 rows as two 32-query column blocks (128 rows and one block
 //   at d = 128, see fwd_q_blocks; at d = 64 a block at the end of a frame with at
 //   most 32 valid rows per wave also runs one column block per wave, see
-//   fwd_rows; a block with at most 32 valid rows in all runs on two waves that
-//   split the keys of every tile, see fwd_tail_rows). Query blocks are frame
-//   aligned, so every row of
+//   fwd_rows; at d = 64 and 96 a block with at most 32 valid rows in all runs on
+//   two waves that split the keys of every tile, see fwd_tail_rows). Query blocks
+//   are frame aligned, so every row of
 //   a workgroup shares one kept list. With a text prefix (the MM-DiT form) the text
 //   is one more segment, see Layout. Workgroup ids are
 //   remapped so that each XCD (8 per MI355X, each with its own L2) receives a
@@ -628,9 +628,8 @@ __device__ __forceinline__ void fwd_rows(int wave, const FwdItem& it, const Layo
 // 1, which take the two 32-key halves of every tile; waves 2 and 3 only load tiles.
 // Wave 1's softmax state (reference, sum, O^T) then joins wave 0's through LDS and
 // wave 0 stores the rows. Each tile costs an active wave a quarter of the matrix and
-// vector work of a full block's wave (half at d = 128, whose full blocks have one
-// column block per wave), so the block frees its workgroup slot early instead of
-// holding it for one wave's whole pass over the tiles.
+// vector work of a full block's wave, so the block frees its workgroup slot early
+// instead of holding it for one wave's whole pass over the tiles.
 template <int D, bool PREFIX, bool TABLE>
 __device__ __forceinline__ void fwd_tail_rows(int wave, const FwdItem& it, const Layout<PREFIX>& lay,
                                               uint16_t (&sK)[2][Shape<D>::kTileElems],
@@ -836,8 +835,11 @@ __device__ __forceinline__ void fwd_unit(
   // waves that split the keys of every tile. Not in the d = 96 kernels with a text
   // prefix or a unit table: their epilogues keep more scalars live across the main
   // tile loop, and with this path as well one of them spills to a vector register,
-  // which pushes a loader offset of the loop (at 256 VGPRs) into scratch memory.
-  if constexpr (D != 96 || (!PREFIX && !TABLE)) {
+  // which pushes a loader offset of the loop (at 256 VGPRs) into scratch memory. Not
+  // at d = 128, whose full blocks already run one column block per wave: there the
+  // short blocks gained nothing, and with dense masks they ran ahead of the full
+  // blocks of their segment, which then took longer per tile.
+  if constexpr (D == 64 || (D == 96 && !PREFIX && !TABLE)) {
     if (it.seg_len - it.qb * kBlockQ <= 32) {
       fwd_tail_rows<D, PREFIX, TABLE>(wave, it, lay, sK, sV, ws_o, ws_lse, lse, ws_parts, c, qflip, qmask);
       return;

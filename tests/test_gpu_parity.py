@@ -272,12 +272,12 @@ SHORT_CASES = [  # (d, T): a last query block of 1 .. 32 rows; T mod 64 sets the
 @pytest.mark.parametrize("form", ["col", "sym"])
 @pytest.mark.parametrize("d,T", SHORT_CASES)
 def test_short_last_query_blocks(d, T, form):
-    """A segment's last query block with at most 32 valid rows runs on two waves, each
-    taking one 32-key half of every tile; the second wave's softmax state joins the
-    first's through LDS. The last key tile of a frame holds 16, 31 or 32 keys here, so
-    the second half is empty or partly masked; with sym masks the heavy frames are
-    split and the short blocks write partials. Every row and the log-sum-exp against
-    the oracle."""
+    """A segment's last query block with at most 32 valid rows runs (at d = 64 and 96)
+    on two waves, each taking one 32-key half of every tile; the second wave's softmax
+    state joins the first's through LDS. The last key tile of a frame holds 16, 31 or
+    32 keys here, so the second half is empty or partly masked; with sym masks the
+    heavy frames are split and the short blocks write partials. At d = 128 the same
+    blocks run on one wave. Every row and the log-sum-exp against the oracle."""
     B, H, F = 1, 3, 7
     qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=T * 3 + d)
     mask = om.tile_mask(F, 2, form)
@@ -486,7 +486,7 @@ PART_CASES = [  # (B, H, F, T, d, g, form): each XCD's last round is cut into pa
     (1, 12, 20, 700, 96, 2, "col"),
     (1, 32, 6, 700, 96, 1, "sym"),
     (1, 8, 11, 700, 128, 1, "col"),
-    # 16-row last query blocks among the parts (keys split over two waves)
+    # 16-row last query blocks among the parts (keys split over two waves at d = 64)
     (1, 32, 6, 528, 64, 1, "col"),
     (1, 20, 6, 528, 128, 1, "col"),
 ]

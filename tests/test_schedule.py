@@ -40,7 +40,7 @@ def test_schedule_covers_every_tile_once(tmp_path):
     # the GPU parity shapes are cut into parts, so those tests cover the merge
     for name in ("gpu-a", "gpu-b", "gpu-c", "gpu-d", "gpu-e", "gpu-f", "gpu-g", "gpu-h"):
         assert got[name][3] > 0, name
-    # among them, short last query blocks (16 rows, two waves splitting the keys)
+    # among them, short last query blocks (16 rows)
     for name in ("gpu-g", "gpu-h"):
         assert got[name][5] > 0, name
     # plans with split frames keep their pieces whole
