@@ -62,6 +62,7 @@
 
 #include "launch.h"
 #include "tile_common.h"
+#include "unit_order.h"
 
 namespace ta {
 namespace {
@@ -775,7 +776,9 @@ __device__ __forceinline__ void fwd_tail_rows(int wave, const FwdItem& it, const
 // a whole unit (slot -1; in a longest-first schedule n_dp_x is 0 and every unit is an
 // entry). sched holds {start_x, n_dp_x, n_tab_x, first entry} per XCD, then the
 // entries. Launches without a table (TABLE false) give XCD x the contiguous units
-// [x q + min(x, r), + q + (x < r)) of the n = q 8 + r units, computed in place.
+// [x q + min(x, r), + q + (x < r)) of the n = q 8 + r units, computed in place, in
+// order, or with the short last blocks of the segments moved to the end of the share
+// (short_last_unit).
 template <int D, bool PREFIX, bool TABLE>
 __device__ __forceinline__ void fwd_unit(
     int wave, uint32_t x, int pos, const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
@@ -792,8 +795,13 @@ __device__ __forceinline__ void fwd_unit(
   it.part = -1;
   uint32_t u;
   if constexpr (!TABLE) {
-    const uint32_t n = (uint32_t)B * per_b, q = n / 8, r = n % 8;
-    u = x * q + min(x, r) + (uint32_t)pos;
+    const uint32_t n = (uint32_t)B * per_b;
+    u = share_start(n, x) + (uint32_t)pos;
+    // Where every segment ends on a short block that runs on two waves (fwd_tail_rows),
+    // the share runs those blocks after its full ones (short_last_unit).
+    if constexpr (!PREFIX && (D == 64 || D == 96)) {
+      if (nqb > 1 && T - (nqb - 1) * kBlockQ <= 32) u = short_last_unit(n, (uint32_t)nqb, x, (uint32_t)pos);
+    }
   } else {
     const int32_t* xi = sched + 4 * x;
     const int n_dp = xi[1];

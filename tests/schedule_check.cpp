@@ -6,14 +6,17 @@
 // one unit, MM-DiT plans list their whole units longest first, and the per-XCD
 // workgroup counts fit the grid. Prints one line per shape:
 // "<name> units U whole W parts P slots S table 0|1 short C", C the units cut into
-// parts whose query block holds at most 32 rows.
+// parts whose query block holds at most 32 rows. It also checks the kernel's order of
+// the units within a share when every segment ends on a short block.
 #include <cstdio>
 #include <cstdlib>
+#include <initializer_list>
 #include <map>
 #include <vector>
 
 #include "host_internal.h"
 #include "tile_attn.h"
+#include "unit_order.h"
 
 using namespace ta::host;
 
@@ -116,6 +119,30 @@ int check(const char* name, int B, int H, int F, int T, int P, int d, int g, int
   return 0;
 }
 
+// The kernel's order of a share whose segments all end on a short block
+// (ta::short_last_unit): every position maps to a distinct unit of the share, the
+// full blocks come first and the short ones last, each in their original order.
+int check_short_last(uint32_t n_items, uint32_t nqb) {
+  const uint32_t n = n_items * nqb;
+  for (uint32_t x = 0; x < 8; ++x) {
+    const uint32_t s = ta::share_start(n, x), cnt = ta::share_count(n, x);
+    std::vector<int> seen(cnt, 0);
+    long prev_full = -1, prev_short = -1;
+    bool in_short = false;
+    for (uint32_t pos = 0; pos < cnt; ++pos) {
+      const uint32_t u = ta::short_last_unit(n, nqb, x, pos);
+      if (u < s || u >= s + cnt || seen[u - s]++) return std::printf("short-last %u %u: bad unit\n", n_items, nqb), 1;
+      const bool is_short = u % nqb == nqb - 1;
+      if (in_short && !is_short) return std::printf("short-last %u %u: full after short\n", n_items, nqb), 1;
+      in_short = is_short;
+      long& prev = is_short ? prev_short : prev_full;
+      if ((long)u <= prev) return std::printf("short-last %u %u: order\n", n_items, nqb), 1;
+      prev = (long)u;
+    }
+  }
+  return 0;
+}
+
 }  // namespace
 
 int main() {
@@ -141,5 +168,12 @@ int main() {
   // short last query blocks (16 rows) among the units cut into parts
   bad |= check("gpu-g", 1, 32, 6, 528, 0, 64, 1, TA_MASK_COL);
   bad |= check("gpu-h", 1, 20, 6, 528, 0, 128, 1, TA_MASK_COL);
+  int orders = 0;
+  for (uint32_t nqb : {2u, 3u, 15u, 29u})
+    for (uint32_t items : {1u, 3u, 7u, 8u, 9u, 57u, 576u, 1153u}) {
+      bad |= check_short_last(items, nqb);
+      ++orders;
+    }
+  std::printf("short-last orders %d\n", orders);
   return bad;
 }

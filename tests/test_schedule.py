@@ -35,6 +35,7 @@ def test_schedule_covers_every_tile_once(tmp_path):
            for m in re.finditer(r"^(\S+) units (\d+) whole (\d+) parts (\d+) slots (\d+) table (\d) short (\d+)$",
                                 res.stdout, re.M)}
     assert len(got) == 17
+    assert "short-last orders 32" in res.stdout
     # a launch whose XCDs run whole rounds only keeps every block whole
     assert got["93f-col"] == (8640, 8640, 0, 0, 0, 0)
     # the GPU parity shapes are cut into parts, so those tests cover the merge
