@@ -186,6 +186,10 @@ void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int 
     const int seg_len = (P > 0 && it[1] == F) ? P : T;
     return (int64_t)(u % nqb) * rows < seg_len;
   };
+  // Where every segment ends on a query block of at most 32 rows (video only, d = 64
+  // or 96), the kernel runs those blocks on two waves, after the full blocks of each
+  // XCD's share, and they already even out the last round: no parts then.
+  const bool short_last = P == 0 && (d == 64 || d == 96) && nqb > 1 && T - (nqb - 1) * rows <= 32;
   std::vector<int32_t> xcd(4 * 8), pieces, cut_units;
   int n_part_slots = 0;
   int64_t wg_max = 0;
@@ -228,7 +232,7 @@ void append_fwd_schedule(HostWorkList& hw, int B, int nqb, int rows, int d, int 
     // even out the last round, and parts of pieces would add a second merge.
     const int64_t ragged = cnt % slots_x;
     int parts_k = 1;
-    if (share_tail && hw.n_heavy == 0 && cnt > slots_x && ragged > 0) {
+    if (share_tail && hw.n_heavy == 0 && !short_last && cnt > slots_x && ragged > 0) {
       double mean_tiles = 0;
       for (int64_t i = cnt - ragged; i < cnt; ++i) mean_tiles += (double)unit_tiles(us[i]);
       mean_tiles /= (double)ragged;

@@ -165,7 +165,8 @@ int main() {
   bad |= check("gpu-e", 1, 12, 9, 1350, 226, 64, 1, TA_MASK_SYM);
   // query frames that keep nothing, some of them in the ragged round cut into parts
   bad |= check("gpu-f", 1, 12, 20, 700, 0, 96, 2, TA_MASK_COL, 7);
-  // short last query blocks (16 rows) among the units cut into parts
+  // short last query blocks (16 rows): at d = 64 run last, no parts; at d = 128 among
+  // the units cut into parts
   bad |= check("gpu-g", 1, 32, 6, 528, 0, 64, 1, TA_MASK_COL);
   bad |= check("gpu-h", 1, 20, 6, 528, 0, 128, 1, TA_MASK_COL);
   int orders = 0;

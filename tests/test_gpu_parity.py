@@ -486,7 +486,8 @@ PART_CASES = [  # (B, H, F, T, d, g, form): each XCD's last round is cut into pa
     (1, 12, 20, 700, 96, 2, "col"),
     (1, 32, 6, 700, 96, 1, "sym"),
     (1, 8, 11, 700, 128, 1, "col"),
-    # 16-row last query blocks among the parts (keys split over two waves at d = 64)
+    # 16-row last query blocks: at d = 64 on two waves, last in each share, no parts;
+    # at d = 128 on one wave, among the parts
     (1, 32, 6, 528, 64, 1, "col"),
     (1, 20, 6, 528, 128, 1, "col"),
 ]
@@ -496,7 +497,8 @@ PART_CASES = [  # (B, H, F, T, d, g, form): each XCD's last round is cut into pa
 def test_ragged_round_in_parts(B, H, F, T, d, g, form):
     """Launches whose XCDs would end on a ragged round of whole query blocks run that
     round's blocks in parts over the kept tiles (merged by log-sum-exp; the host check
-    in tests/test_schedule.py confirms these shapes are cut). Sampled rows of every
+    in tests/test_schedule.py confirms these shapes are cut, all but the d = 64 one with
+    16-row last blocks, which runs those blocks last instead). Sampled rows of every
     frame and head, and the log-sum-exp of two heads, against the oracle."""
     print(f"[case] parts B={B} H={H} F={F} T={T} d={d} {form} g={g}", flush=True)
     qb, kb, vb = workloads.make_qkv(B, H, F, T, d, seed=F * T + d)

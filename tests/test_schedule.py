@@ -39,11 +39,14 @@ def test_schedule_covers_every_tile_once(tmp_path):
     # a launch whose XCDs run whole rounds only keeps every block whole
     assert got["93f-col"] == (8640, 8640, 0, 0, 0, 0)
     # the GPU parity shapes are cut into parts, so those tests cover the merge
-    for name in ("gpu-a", "gpu-b", "gpu-c", "gpu-d", "gpu-e", "gpu-f", "gpu-g", "gpu-h"):
+    for name in ("gpu-a", "gpu-b", "gpu-c", "gpu-d", "gpu-e", "gpu-f", "gpu-h"):
         assert got[name][3] > 0, name
-    # among them, short last query blocks (16 rows)
-    for name in ("gpu-g", "gpu-h"):
-        assert got[name][5] > 0, name
+    # among them, short last query blocks (16 rows, d = 128)
+    assert got["gpu-h"][5] > 0
+    # where every segment ends on a short block at d = 64 or 96 (video only), the kernel
+    # runs those blocks last in each share and the schedule cuts no parts
+    for name in ("gpu-g", "29f-col", "sp-col", "93f-col"):
+        assert got[name][2] == 0 and got[name][4] == 0, name
     # plans with split frames keep their pieces whole
     for name in ("sp-sym", "cog-sym"):
         assert got[name][2] == 0, name
