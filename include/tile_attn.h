@@ -46,7 +46,9 @@
  *     frame, that round's query blocks are cut into parts over their kept tiles,
  *     n_parts * R * (d + 4) * 4 bytes (R = 256 query rows per block, 128 at
  *     d = 128; n_parts is at most 16 per block cut, and zero when the launch
- *     fills whole rounds). An MM-DiT forward at d = 64 whose plan splits frames
+ *     fills whole rounds, and for video-only calls at d = 64 and 96 whose frames
+ *     end on a block of at most 32 rows, which run those blocks last instead).
+ *     An MM-DiT forward at d = 64 whose plan splits frames
  *     also uses 256 bytes of work-queue counters, allocated and zeroed
  *     (synchronously) by the first such call on a stream; every call leaves them
  *     zero. The workspace is held per (device, stream). A call that needs more
